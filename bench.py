@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark: the batched heterogeneous-adapter LoRA apply on one MI355X.
+
+One step = one pass of the whole hot path over one batch already resident in
+HBM: plora_segment (group the batch's tokens by adapter) then plora_apply
+(y += s_i (x A_i) B_i for every token, one launch).  Each step takes a fresh
+token-to-adapter draw from a pool drawn up front, and a different replica of
+the adapter stack, so that an adapter's bytes are never still sitting in the
+256 MB Infinity Cache from an earlier step (a served model revisits one
+projection's stack only after every other LoRA projection of every layer).
+
+Prints ONE JSON line.  ``value`` is whole-job tokens/s over the timed steps
+(wall clock, segment + apply).  ``roofline`` prices the dominant kernel,
+plora_apply: algorithmic bytes per launch (distinct adapters' A_i and B_i,
+2 r_i (h_in + h_out) bytes each, plus x read, y read and written, and the
+token permutation) over its average duration from HIP events recorded on the
+launch stream.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
+the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0
+MALL_BYTES = 256 << 20
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="decode",
+                    choices=["tiny", "decode", "large", "ragged", "prefill"])
+    ap.add_argument("--draws", type=int, default=64,
+                    help="distinct token-to-adapter draws cycled through")
+    ap.add_argument("--replicas", type=int, default=0,
+                    help="adapter-stack replicas rotated per step (0 = auto)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceiling", action="store_true")
+    return ap.parse_args()
+
+
+def describe(name, c):
+    if name == "prefill":
+        return (f"prefill+decode: {c.n_req} requests of U{{1..{c.max_len}}} tokens, "
+                f"one adapter each of N={c.N}; h_in={c.h_in}, h_out={c.h_out}, "
+                f"r={c.rank}, bf16")
+    rank = "U{" + ",".join(map(str, c.rank)) + "}" if isinstance(c.rank, tuple) else c.rank
+    dist = f"Zipf({c.alpha})" if c.dist == "zipf" else c.dist
+    return (f"{name}: T={c.T} tokens, h_in={c.h_in}, h_out={c.h_out}, r={rank}, "
+            f"N={c.N} bf16 adapters, ids {dist}")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the apply has no multi-GPU path in this build).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_05483_amd import plora as P
+    from paper_2608_05483_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    name = args.config
+    c = W.CONFIGS[name]
+    seed = 1000 + W.CONFIG_NAMES.index(name)
+    w = W.make_workload(name)
+    N = w.n_adapters
+
+    # ---- token-to-adapter draws -------------------------------------------------
+    draws = [W.draw_idx(name, seed, d) for d in range(args.draws)]
+    Tmax = max(d.size for d in draws)
+    act_bytes = lambda T: T * (2 * w.h_in + 4 * w.h_out) + 4 * T
+    ad_bytes = [W.adapter_bytes(w.ranks, d, w.h_in, w.h_out, N) for d in draws]
+    tot_bytes = [a + act_bytes(d.size) for a, d in zip(ad_bytes, draws)]
+
+    # ---- device buffers -----------------------------------------------------------
+    base = P.Adapters.from_workload(w, device=dev)
+    stack_bytes = 2 * (base.A.numel() + base.B.numel())
+    R = args.replicas
+    if R <= 0:
+        per_step = max(1, int(np.mean(ad_bytes)))
+        R = max(2, min(64, math.ceil(3 * MALL_BYTES / per_step)))
+        R = max(1, min(R, int((96 << 30) // max(stack_bytes, 1))))
+    reps = [base]
+    for _ in range(R - 1):
+        reps.append(P.Adapters(base.A.clone(), base.B.clone(), base.a_off, base.b_off,
+                               base.ranks, base.scales, w.h_in, w.h_out, base.max_rank))
+    xw = w if Tmax == w.T else W.with_idx(w, np.zeros(Tmax, np.int32))
+    x = torch.from_numpy(xw.x).view(torch.int16).to(dev)
+    y_host = np.zeros((Tmax, w.h_out), np.uint16)
+    n = min(Tmax, w.T)
+    y_host[:n] = w.y_base[:n]
+    y = torch.from_numpy(y_host).view(torch.int16).to(dev)
+    ws = P.Workspace(Tmax, base)
+    idx_dev = [torch.from_numpy(d).to(dev) for d in draws]
+    segs = [P.Segments(d.size, N, device=dev) for d in draws]
+
+    def step(k, ev=None):
+        d = k % len(draws)
+        T = draws[d].size
+        P.segment(idx_dev[d], segs[d])
+        if ev is not None:
+            ev[0].record()
+        P.apply(x[:T], reps[k % R], segs[d], y[:T], ws)
+        if ev is not None:
+            ev[1].record()
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        step(args.warmup + k, evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    apply_ms = np.array([a.elapsed_time(b) for a, b in evs])
+    ks = [(args.warmup + k) % len(draws) for k in range(K)]
+    tokens = sum(draws[d].size for d in ks)
+    bytes_total = sum(tot_bytes[d] for d in ks)
+    bytes_adapter = sum(ad_bytes[d] for d in ks)
+    apply_s = apply_ms.sum() / 1e3
+    achieved = bytes_total / apply_s / 1e9
+    adapter_gbps = bytes_adapter / apply_s / 1e9
+    fallbacks = ws.fallbacks()
+
+    # ---- same-footprint plain-read ceiling -------------------------------------
+    ceiling = None
+    if not args.no_ceiling:
+        import ctypes
+        from paper_2608_05483_amd import build as B
+        pl = ctypes.CDLL(B.PROBE_LIB)
+        pl.plora_probe_read.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int32] * 3 + \
+            [ctypes.c_void_p] * 2
+        pl.plora_probe_sink_words.argtypes = [ctypes.c_int32]
+        uniq = [torch.from_numpy(np.unique(d[(d >= 0) & (d < N)]).astype(np.int32)).to(dev)
+                for d in draws]
+        sink = torch.empty(pl.plora_probe_sink_words(max(u.numel() for u in uniq)),
+                           dtype=torch.int32, device=dev)
+        stream = torch.cuda.current_stream().cuda_stream
+        pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(K)]
+        for k in range(K + args.warmup):
+            d = k % len(draws)
+            rp = reps[k % R]
+            e = pev[k - args.warmup] if k >= args.warmup else None
+            if e:
+                e[0].record()
+            rc = pl.plora_probe_read(rp.A.data_ptr(), rp.B.data_ptr(), rp.a_off.data_ptr(),
+                                     rp.b_off.data_ptr(), rp.ranks.data_ptr(),
+                                     uniq[d].data_ptr(), uniq[d].numel(), w.h_in, w.h_out,
+                                     sink.data_ptr(), stream)
+            assert rc == 0
+            if e:
+                e[1].record()
+        torch.cuda.synchronize()
+        read_s = sum(a.elapsed_time(b) for a, b in pev) / 1e3
+        ceiling = {"kernel": "plain 128-bit read of the same adapter blocks",
+                   "GBps": round(bytes_adapter / read_s / 1e9, 1),
+                   "us_per_launch": round(read_s / K * 1e6, 3),
+                   "frac_of_peak": round(bytes_adapter / read_s / 1e9 / HBM_PEAK_GBPS, 4)}
+
+    # ---- CPU oracle baseline ----------------------------------------------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+        import oracle
+        cores = len(os.sched_getaffinity(0))
+        n_done, toks, t_cpu = 0, 0, 0.0
+        while t_cpu < args.cpu_seconds and n_done < len(draws):
+            d = draws[n_done]
+            wd = w if d.size == w.T else W.with_idx(w, d)
+            t1 = time.perf_counter()
+            oracle.apply(wd.x, d, w.A, w.a_off, w.B, w.b_off, w.ranks, w.scales,
+                         wd.y_base, w.h_in, w.h_out, n_threads=cores)
+            t_cpu += time.perf_counter() - t1
+            toks += d.size
+            n_done += 1
+        cpu = {"value": round(toks / t_cpu, 1), "unit": "tokens/s", "cores": cores,
+               "kind": "oracle",
+               "sample": f"{n_done} batches of this workload ({toks} tokens, "
+                         f"{t_cpu:.1f} s), fp32 C oracle, OpenMP over tokens"}
+
+    out = {
+        "metric": "tokens/s and effective adapter GB/s (% of HBM peak) for plora_apply",
+        "value": round(tokens / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / K * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": describe(name, c), "T": int(Tmax), "h_in": w.h_in,
+                   "h_out": w.h_out, "max_rank": w.max_rank, "n_adapters": N,
+                   "draws": len(draws), "stack_replicas": R},
+        "adapter_GBps": round(adapter_gbps, 1),
+        "adapter_frac_of_peak": round(adapter_gbps / HBM_PEAK_GBPS, 4),
+        "apply_us": round(float(apply_ms.mean()) * 1e3, 3),
+        "apply_us_p10_p90": [round(float(np.percentile(apply_ms, 10)) * 1e3, 3),
+                             round(float(np.percentile(apply_ms, 90)) * 1e3, 3)],
+        "bytes_per_launch": int(bytes_total / K),
+        "adapter_bytes_per_launch": int(bytes_adapter / K),
+        "fallbacks": int(fallbacks),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+        "read_ceiling": ceiling,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

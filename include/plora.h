@@ -1,0 +1,238 @@
+/*
+ * plora.h -- C ABI of the MI355X (gfx950) batched heterogeneous-adapter LoRA
+ * apply, the hot path of multi-LoRA serving in PLoRA.
+ *
+ * The operation (paper section II-A: a LoRA layer computes y = x(W + AB) with
+ * A: D1 x R and B: R x D2; section II-B: one shared base model serves many
+ * adapters, each request using its own; section V-A: strategies E1..E4 all
+ * compute y = xAB, E4 by shipping the rank-R intermediate m = xA and forming
+ * y = mB afterwards):
+ *
+ *   y[t, :] = y_base[t, :] + s_i * (x[t, :] A_i) B_i,   i = idx[t]
+ *
+ * for a batch of T tokens, each naming one of N adapters.  y_base = x W is the
+ * base projection, produced by the caller; every call below accumulates into
+ * y in place (y holds y_base on entry).  s_i is a per-adapter scale (s_i = 1
+ * is the paper's formula).
+ *
+ * The work is split the way the paper's cost model groups it (section VI-B):
+ * tokens are first grouped per adapter (the per-adapter batch B_i), and each
+ * adapter's A_i and B_i are then read once per call whatever its batch size.
+ *
+ *   plora_segment  group tokens by adapter id (stable counting sort)
+ *   plora_shrink   v[t, :] = x[t, :] A_i            (E4's m = xA, fp32)
+ *   plora_expand   y[t, :] += s_i v[t, :] B_i        (E4's y = mB)
+ *   plora_apply    both in one launch; v never leaves the chip's caches
+ *
+ * Data types and layouts (all row-major, element strides):
+ *   x       bf16 [T, ldx], first h_in columns used
+ *   y       bf16 [T, ldy], first h_out columns used, read and written
+ *   v       fp32 [T, ldv], columns c < r_i of valid tokens defined
+ *   A stack bf16, A_i = h_in x r_i at element offset a_off[i]
+ *   B stack bf16, B_i = r_i x h_out at element offset b_off[i]
+ *   bf16 values are passed as their 16-bit patterns (uint16_t).
+ * Arithmetic: bf16 x bf16 products are exact in fp32; all sums are fp32;
+ * v is never rounded below fp32; y is rounded once, to nearest even.
+ * Reduction orders are fixed, so every call is bitwise deterministic, and
+ * plora_apply equals plora_shrink followed by plora_expand bit for bit.
+ *
+ * Memory and ownership: every pointer below is a DEVICE pointer unless the
+ * text says "host"; the caller allocates and owns every buffer.  No call
+ * allocates device memory, synchronizes the device or the stream, or keeps a
+ * pointer after it returns (plora_check_adapters alone copies to the host and
+ * waits).  Every launch goes onto the caller's stream.
+ *
+ * Errors: a call returns PLORA_OK or an error before launching anything,
+ * except PLORA_ERR_HIP, which reports a failed launch.  Rules:
+ *   PLORA_ERR_INVALID_ARG      null required pointer, negative size, a leading
+ *                              dimension below the row width, or a segments
+ *                              struct whose sizes do not match T and N
+ *   PLORA_ERR_UNSUPPORTED      h_in or h_out not a multiple of 8; max_rank not
+ *                              a multiple of 8 or above PLORA_MAX_RANK; a
+ *                              pointer not 16-byte aligned; ldx/ldy not a
+ *                              multiple of 8 or ldv not a multiple of 4;
+ *                              T above PLORA_MAX_TOKENS; (N+1) * 2^ceil(log2 T)
+ *                              beyond 2^32
+ *   PLORA_ERR_WORKSPACE_TOO_SMALL  ws_bytes below plora_workspace_bytes()
+ *   PLORA_ERR_HIP              a launch failed (hipGetLastError)
+ * T == 0 launches nothing, writes nothing and returns PLORA_OK.
+ * Conditions only the device can see never trap: a token whose idx is -1
+ * (no adapter) or outside [0, N) keeps y_base and is counted in meta; an
+ * adapter whose rank is 0 is a no-op; an adapter whose rank is not a
+ * multiple of 8, exceeds max_rank, or whose A_i/B_i block is misaligned or
+ * runs past a_len/b_len is skipped (its tokens keep y_base) --
+ * plora_check_adapters reports such entries on the host.
+ * Calls that share a workspace or a segments struct must not overlap in time
+ * (same stream, or externally ordered).
+ */
+#ifndef PLORA_H
+#define PLORA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PLORA_OK = 0,
+  PLORA_ERR_INVALID_ARG = 1,
+  PLORA_ERR_UNSUPPORTED = 2,
+  PLORA_ERR_WORKSPACE_TOO_SMALL = 3,
+  PLORA_ERR_HIP = 4
+} plora_status;
+
+/* Largest adapter rank (the paper's rank range is 2..128, section V-A). */
+#define PLORA_MAX_RANK 128
+/* Largest token batch one plora_segment call groups. */
+#define PLORA_MAX_TOKENS 16384
+/* Tokens per work tile; a segment longer than this is split into tiles. */
+#define PLORA_TILE_TOKENS 32
+/* Entries of plora_segments.meta. */
+#define PLORA_META_WORDS 8
+
+/*
+ * The adapter stack.  Host struct; the pointers inside are device pointers.
+ *   n_adapters  N, number of adapters (ids 0..N-1)
+ *   h_in, h_out model dimensions D1, D2 (multiples of 8)
+ *   max_rank    host upper bound on every ranks[i] (multiple of 8, <= 128);
+ *               sizes the workspace and the v stride
+ *   A, B        flat bf16 stacks of a_len and b_len elements
+ *   a_off,b_off int64 [N] element offsets of A_i and B_i (multiples of 8)
+ *   ranks       int32 [N], r_i in {0, 8, 16, ..., max_rank}
+ *   scales      fp32  [N], s_i
+ * Ranks that are not multiples of 8 are not supported: an adapter of rank
+ * r < 8k is stored with its A_i columns and B_i rows zero-padded to the next
+ * multiple of 8, which leaves every result unchanged.
+ */
+typedef struct {
+  int32_t n_adapters;
+  int32_t h_in;
+  int32_t h_out;
+  int32_t max_rank;
+  const uint16_t* A;
+  const uint16_t* B;
+  int64_t a_len;
+  int64_t b_len;
+  const int64_t* a_off;
+  const int64_t* b_off;
+  const int32_t* ranks;
+  const float* scales;
+} plora_adapters;
+
+/*
+ * The grouping of one token batch, written by plora_segment and read by the
+ * other calls.  Host struct; the arrays are device memory owned by the caller.
+ *   T          tokens in the batch (host)
+ *   cap        min(T, N) (host), the most segments a batch can have
+ *   tile_cap   plora_tile_capacity(T, N) (host)
+ *   perm       int32 [T]: token indices of valid tokens, grouped by adapter
+ *              (ascending id, ascending token index inside a group); -1 after
+ *              the n_valid-th entry
+ *   seg_ptr    int32 [cap+1]: start of each segment in perm; entries past
+ *              the last segment hold n_valid
+ *   seg_id     int32 [cap]: adapter id of each segment; -1 past the last
+ *   meta       int32 [PLORA_META_WORDS]: {n_seg, n_valid, n_none (idx == -1),
+ *              n_invalid (other ids outside [0, N)), n_tiles, 0, 0, 0}
+ *   tiles      int32 [tile_cap][4]: the work tiles of the apply kernels,
+ *              {adapter id, first perm position, length, segment index};
+ *              a segment of L tokens gives ceil(L / PLORA_TILE_TOKENS) tiles;
+ *              unused entries hold {-1, 0, 0, -1}
+ * One segmentation serves every projection and layer of a step that shares
+ * the token batch.
+ */
+typedef struct {
+  int32_t T;
+  int32_t cap;
+  int32_t tile_cap;
+  int32_t reserved;
+  int32_t* perm;
+  int32_t* seg_ptr;
+  int32_t* seg_id;
+  int32_t* meta;
+  int32_t* tiles;
+} plora_segments;
+
+/* Host.  min(T, cap + T / PLORA_TILE_TOKENS) with cap = min(T, N): the most
+ * tiles a batch of T tokens over N adapters can produce; 0 for T <= 0. */
+int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
+
+/* Host.  Bytes of device workspace plora_shrink / plora_apply need for a
+ * batch of T tokens over this adapter stack (only the host scalars of *ad are
+ * read).  plora_segment and plora_expand need none. */
+size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad);
+
+/* Zero a workspace before its first use (it is left zeroed by every call
+ * afterwards, so this is needed once per allocation).  Enqueued on stream. */
+plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Group the batch: idx is int32 [T] device memory; fills seg->perm, seg_ptr,
+ * seg_id, meta and tiles (seg->T, cap and tile_cap must be set).  This is the
+ * per-adapter batch of the cost model (section VI-B).  ws may be NULL.
+ * Bitwise deterministic; equal ids keep their token order.
+ */
+plora_status plora_segment(const int32_t* idx, const plora_segments* seg,
+                           int32_t n_adapters, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/*
+ * v[t, c] = sum_k x[t, k] * A_i[k, c] for every valid token t and c < r_i
+ * (the rank-r reduction m = xA of strategy E4, section V-A).  Entries of v
+ * for other tokens and columns are not written.  Needs the workspace.
+ */
+plora_status plora_shrink(const uint16_t* x, int64_t ldx,
+                          const plora_adapters* ad, const plora_segments* seg,
+                          float* v, int64_t ldv, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/*
+ * y[t, j] = bf16(y[t, j] + s_i * sum_c v[t, c] * B_i[c, j]) for every valid
+ * token t (the expand y = mB of strategy E4), in place.  ws may be NULL.
+ */
+plora_status plora_expand(const float* v, int64_t ldv,
+                          const plora_adapters* ad, const plora_segments* seg,
+                          uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/*
+ * The fused apply, one launch: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for
+ * every valid token (strategy E1: both matrices resident in GPU memory,
+ * section V-A).  x and y must not overlap.  Needs the workspace.
+ */
+plora_status plora_apply(const uint16_t* x, int64_t ldx,
+                         const plora_adapters* ad, const plora_segments* seg,
+                         uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+/*
+ * Host, synchronous (copies ranks and offsets to the host and waits on
+ * stream).  Returns PLORA_OK if every adapter entry is usable by the kernels
+ * (rank 0 or a multiple of 8 up to max_rank; offsets multiples of 8; blocks
+ * inside a_len / b_len), else PLORA_ERR_INVALID_ARG with the first bad
+ * adapter index in *bad_index (may be NULL).  Not for the hot path.
+ */
+plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
+                                  hipStream_t stream);
+
+/* Static string naming a status code. */
+const char* plora_status_string(plora_status status);
+
+/*
+ * Test hooks.  plora_debug_set_spin_limit sets, process-wide, how many polls
+ * a fused-apply work group makes on its tile's arrival counter before it
+ * stops waiting and recomputes the tile's whole x A_i itself (bitwise the
+ * same result); 0 restores the default.  plora_debug_fallbacks reads how many
+ * work groups took that path, from a workspace (synchronous copy).
+ */
+void plora_debug_set_spin_limit(int32_t polls);
+int64_t plora_debug_fallbacks(const void* ws, size_t ws_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PLORA_H */

@@ -1,0 +1,257 @@
+"""Thin Python binding of ``libplora.so`` (include/plora.h).
+
+Argument marshalling only: every function forwards raw device pointers,
+sizes and the caller's HIP stream to the C ABI of the same name and raises
+``PloraError`` on a non-OK status.  torch is used for device memory and
+streams; the helper classes at the bottom allocate the buffers a call needs
+as torch tensors and fill the ABI structs from them.
+
+Importing this module loads the HIP library and fails loudly if it has not
+been built (``python -m paper_2608_05483_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+from . import build as _build
+
+PLORA_OK = 0
+PLORA_ERR_INVALID_ARG = 1
+PLORA_ERR_UNSUPPORTED = 2
+PLORA_ERR_WORKSPACE_TOO_SMALL = 3
+PLORA_ERR_HIP = 4
+PLORA_MAX_RANK = 128
+PLORA_MAX_TOKENS = 16384
+PLORA_TILE_TOKENS = 32
+PLORA_META_WORDS = 8
+
+EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
+            "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
+            "plora_check_adapters", "plora_status_string",
+            "plora_debug_set_spin_limit", "plora_debug_fallbacks")
+
+
+class PloraError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn}: {status_string(status)}")
+        self.status = status
+
+
+class plora_adapters(ctypes.Structure):
+    _fields_ = [("n_adapters", ctypes.c_int32), ("h_in", ctypes.c_int32),
+                ("h_out", ctypes.c_int32), ("max_rank", ctypes.c_int32),
+                ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
+                ("a_len", ctypes.c_int64), ("b_len", ctypes.c_int64),
+                ("a_off", ctypes.c_void_p), ("b_off", ctypes.c_void_p),
+                ("ranks", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
+class plora_segments(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("cap", ctypes.c_int32),
+                ("tile_cap", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("perm", ctypes.c_void_p), ("seg_ptr", ctypes.c_void_p),
+                ("seg_id", ctypes.c_void_p), ("meta", ctypes.c_void_p),
+                ("tiles", ctypes.c_void_p)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(_build.LIB):
+        raise ImportError(
+            f"{_build.LIB} is not built; run `python -m paper_2608_05483_amd.build`")
+    L = ctypes.CDLL(_build.LIB)
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    AD, SG = ctypes.POINTER(plora_adapters), ctypes.POINTER(plora_segments)
+    L.plora_tile_capacity.argtypes = [i32, i32]
+    L.plora_tile_capacity.restype = i32
+    L.plora_workspace_bytes.argtypes = [i32, AD]
+    L.plora_workspace_bytes.restype = sz
+    L.plora_workspace_init.argtypes = [P, sz, P]
+    L.plora_segment.argtypes = [P, SG, i32, P, sz, P]
+    L.plora_shrink.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_expand.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_apply.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_check_adapters.argtypes = [AD, ctypes.POINTER(i32), P]
+    L.plora_status_string.argtypes = [ctypes.c_int]
+    L.plora_status_string.restype = ctypes.c_char_p
+    L.plora_debug_set_spin_limit.argtypes = [i32]
+    L.plora_debug_set_spin_limit.restype = None
+    L.plora_debug_fallbacks.argtypes = [P, sz, P]
+    L.plora_debug_fallbacks.restype = i64
+    for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
+               "plora_expand", "plora_apply", "plora_check_adapters"):
+        getattr(L, fn).restype = ctypes.c_int
+    return L
+
+
+lib = _load()
+LIB_PATH = _build.LIB
+
+
+def _ok(fn: str, status: int) -> None:
+    if status != PLORA_OK:
+        raise PloraError(fn, status)
+
+
+def status_string(status: int) -> str:
+    return lib.plora_status_string(status).decode()
+
+
+# ---- the C ABI, one Python function per entry point -------------------------
+
+def plora_tile_capacity(T: int, n_adapters: int) -> int:
+    return int(lib.plora_tile_capacity(T, n_adapters))
+
+
+def plora_workspace_bytes(T: int, ad: plora_adapters) -> int:
+    return int(lib.plora_workspace_bytes(T, ctypes.byref(ad)))
+
+
+def plora_workspace_init(ws: int, ws_bytes: int, stream: int) -> None:
+    _ok("plora_workspace_init", lib.plora_workspace_init(ws, ws_bytes, stream))
+
+
+def plora_segment(idx: int, seg: plora_segments, n_adapters: int, ws: int | None,
+                  ws_bytes: int, stream: int) -> None:
+    _ok("plora_segment", lib.plora_segment(idx, ctypes.byref(seg), n_adapters, ws,
+                                           ws_bytes, stream))
+
+
+def plora_shrink(x: int, ldx: int, ad: plora_adapters, seg: plora_segments, v: int,
+                 ldv: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _ok("plora_shrink", lib.plora_shrink(x, ldx, ctypes.byref(ad), ctypes.byref(seg),
+                                         v, ldv, ws, ws_bytes, stream))
+
+
+def plora_expand(v: int, ldv: int, ad: plora_adapters, seg: plora_segments, y: int,
+                 ldy: int, ws: int | None, ws_bytes: int, stream: int) -> None:
+    _ok("plora_expand", lib.plora_expand(v, ldv, ctypes.byref(ad), ctypes.byref(seg),
+                                         y, ldy, ws, ws_bytes, stream))
+
+
+def plora_apply(x: int, ldx: int, ad: plora_adapters, seg: plora_segments, y: int,
+                ldy: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _ok("plora_apply", lib.plora_apply(x, ldx, ctypes.byref(ad), ctypes.byref(seg),
+                                       y, ldy, ws, ws_bytes, stream))
+
+
+def plora_check_adapters(ad: plora_adapters, stream: int) -> int:
+    """-1 if every adapter entry is usable, else the first bad index."""
+    bad = ctypes.c_int32(-1)
+    st = lib.plora_check_adapters(ctypes.byref(ad), ctypes.byref(bad), stream)
+    if st == PLORA_ERR_INVALID_ARG and bad.value >= 0:
+        return bad.value
+    _ok("plora_check_adapters", st)
+    return -1
+
+
+def plora_debug_set_spin_limit(polls: int) -> None:
+    lib.plora_debug_set_spin_limit(polls)
+
+
+def plora_debug_fallbacks(ws: int, ws_bytes: int, stream: int) -> int:
+    return int(lib.plora_debug_fallbacks(ws, ws_bytes, stream))
+
+
+# ---- torch-backed buffers ----------------------------------------------------
+
+def _stream(stream=None) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+class Adapters:
+    """Device-resident adapter stack and its ABI struct."""
+
+    def __init__(self, A, B, a_off, b_off, ranks, scales, h_in: int, h_out: int,
+                 max_rank: int):
+        self.A, self.B = A, B
+        self.a_off, self.b_off, self.ranks, self.scales = a_off, b_off, ranks, scales
+        self.h_in, self.h_out, self.max_rank = h_in, h_out, max_rank
+        self.n_adapters = int(ranks.numel())
+        self.struct = plora_adapters(
+            self.n_adapters, h_in, h_out, max_rank, A.data_ptr(), B.data_ptr(),
+            A.numel(), B.numel(), a_off.data_ptr(), b_off.data_ptr(),
+            ranks.data_ptr(), scales.data_ptr())
+
+    @classmethod
+    def from_arrays(cls, A, B, a_off, b_off, ranks, scales, h_in, h_out,
+                    max_rank=None, device="cuda"):
+        import numpy as np
+        import torch
+        t = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to(device=device,
+                                                                       dtype=dt)
+        ranks_np = np.asarray(ranks, np.int32)
+        if max_rank is None:
+            mr = int(ranks_np.max()) if ranks_np.size else 8
+            max_rank = max(8, (mr + 7) // 8 * 8)
+        return cls(t(np.asarray(A, np.uint16).view(np.int16), torch.int16),
+                   t(np.asarray(B, np.uint16).view(np.int16), torch.int16),
+                   t(np.asarray(a_off, np.int64), torch.int64),
+                   t(np.asarray(b_off, np.int64), torch.int64),
+                   t(ranks_np, torch.int32), t(np.asarray(scales, np.float32),
+                                               torch.float32),
+                   h_in, h_out, max_rank)
+
+    @classmethod
+    def from_workload(cls, w, device="cuda"):
+        return cls.from_arrays(w.A, w.B, w.a_off, w.b_off, w.ranks, w.scales,
+                               w.h_in, w.h_out, device=device)
+
+
+class Segments:
+    """Device buffers of one token batch's grouping and its ABI struct."""
+
+    def __init__(self, T: int, n_adapters: int, device="cuda"):
+        import torch
+        self.T, self.n_adapters = T, n_adapters
+        self.cap = min(T, n_adapters)
+        self.tile_cap = plora_tile_capacity(T, n_adapters)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.perm = torch.empty(max(T, 1), **i32)
+        self.seg_ptr = torch.empty(self.cap + 1, **i32)
+        self.seg_id = torch.empty(max(self.cap, 1), **i32)
+        self.meta = torch.zeros(PLORA_META_WORDS, **i32)
+        self.tiles = torch.empty(max(self.tile_cap, 1) * 4, **i32)
+        self.struct = plora_segments(T, self.cap, self.tile_cap, 0,
+                                     self.perm.data_ptr(), self.seg_ptr.data_ptr(),
+                                     self.seg_id.data_ptr(), self.meta.data_ptr(),
+                                     self.tiles.data_ptr())
+
+
+class Workspace:
+    """Zero-initialised workspace sized for (T, adapter stack)."""
+
+    def __init__(self, T: int, ad: Adapters, device="cuda", stream=None):
+        import torch
+        self.nbytes = plora_workspace_bytes(T, ad.struct)
+        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+        plora_workspace_init(self.buf.data_ptr(), self.nbytes, _stream(stream))
+
+    @property
+    def ptr(self) -> int:
+        return self.buf.data_ptr()
+
+    def fallbacks(self, stream=None) -> int:
+        return plora_debug_fallbacks(self.ptr, self.nbytes, _stream(stream))
+
+
+def segment(idx, segs: Segments, stream=None) -> None:
+    plora_segment(idx.data_ptr(), segs.struct, segs.n_adapters, None, 0,
+                  _stream(stream))
+
+
+def shrink(x, ad: Adapters, segs: Segments, v, ws: Workspace, stream=None) -> None:
+    plora_shrink(x.data_ptr(), x.stride(0), ad.struct, segs.struct, v.data_ptr(),
+                 v.stride(0), ws.ptr, ws.nbytes, _stream(stream))
+
+
+def expand(v, ad: Adapters, segs: Segments, y, stream=None) -> None:
+    plora_expand(v.data_ptr(), v.stride(0), ad.struct, segs.struct, y.data_ptr(),
+                 y.stride(0), None, 0, _stream(stream))
+
+
+def apply(x, ad: Adapters, segs: Segments, y, ws: Workspace, stream=None) -> None:
+    plora_apply(x.data_ptr(), x.stride(0), ad.struct, segs.struct, y.data_ptr(),
+                y.stride(0), ws.ptr, ws.nbytes, _stream(stream))

@@ -1,0 +1,156 @@
+"""The C ABI library without a GPU: it loads, exports every entry point the
+header declares, and its host-side argument checks return the documented
+status codes before anything is launched."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_05483_amd import build as B
+from paper_2608_05483_amd import plora as P
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "plora.h")
+
+FAKE = 0x10000  # an aligned non-null address; never dereferenced by these checks
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(plora_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_expected_calls():
+    names = declared_functions()
+    for fn in ("plora_segment", "plora_shrink", "plora_expand", "plora_apply",
+               "plora_workspace_bytes", "plora_status_string"):
+        assert fn in names
+    assert set(names) == set(P.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(B.LIB)
+    for fn in declared_functions():
+        assert hasattr(lib, fn), fn
+
+
+def test_status_strings():
+    assert P.status_string(P.PLORA_OK) == "PLORA_OK"
+    assert P.status_string(P.PLORA_ERR_HIP) == "PLORA_ERR_HIP"
+    assert P.status_string(99) == "PLORA_ERR_UNKNOWN"
+
+
+def test_tile_capacity():
+    assert P.plora_tile_capacity(0, 10) == 0
+    assert P.plora_tile_capacity(64, 1000) == 64
+    assert P.plora_tile_capacity(8192, 32) == 32 + 8192 // 32
+    assert P.plora_tile_capacity(5, 1) == 1
+    # the bound holds for the worst batch: every segment of length 32k+1
+    for T, N in [(100, 3), (1000, 7), (16384, 1000)]:
+        cap = min(T, N)
+        assert P.plora_tile_capacity(T, N) >= min(T, cap + T // 32)
+
+
+def _ad(**kw):
+    a = dict(n_adapters=4, h_in=256, h_out=256, max_rank=8, A=FAKE, B=FAKE,
+             a_len=4 * 256 * 8, b_len=4 * 256 * 8, a_off=FAKE, b_off=FAKE,
+             ranks=FAKE, scales=FAKE)
+    a.update(kw)
+    return P.plora_adapters(**a)
+
+
+def _seg(T=8, N=4, **kw):
+    s = dict(T=T, cap=min(T, N), tile_cap=P.plora_tile_capacity(T, N), reserved=0,
+             perm=FAKE, seg_ptr=FAKE, seg_id=FAKE, meta=FAKE, tiles=FAKE)
+    s.update(kw)
+    return P.plora_segments(**s)
+
+
+def _apply_status(ad=None, seg=None, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
+                  ws_bytes=None):
+    ad = ad or _ad()
+    seg = seg or _seg()
+    if ws_bytes is None:
+        ws_bytes = P.plora_workspace_bytes(seg.T, ad)
+    return P.lib.plora_apply(x, ldx, ctypes.byref(ad), ctypes.byref(seg), y, ldy, ws,
+                             ws_bytes, None)
+
+
+def test_workspace_size_is_checked():
+    ad = _ad()
+    need = P.plora_workspace_bytes(8, ad)
+    assert need > 0
+    assert _apply_status(ws_bytes=need - 1) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
+    assert _apply_status(ws=None) == P.PLORA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h_in=260), P.PLORA_ERR_UNSUPPORTED),
+    (dict(h_out=12), P.PLORA_ERR_UNSUPPORTED),
+    (dict(max_rank=12), P.PLORA_ERR_UNSUPPORTED),
+    (dict(max_rank=136), P.PLORA_ERR_UNSUPPORTED),
+    (dict(max_rank=0), P.PLORA_ERR_UNSUPPORTED),
+    (dict(h_in=0), P.PLORA_ERR_INVALID_ARG),
+    (dict(A=None), P.PLORA_ERR_INVALID_ARG),
+    (dict(A=FAKE + 2), P.PLORA_ERR_UNSUPPORTED),
+    (dict(n_adapters=-1), P.PLORA_ERR_INVALID_ARG),
+])
+def test_adapter_checks(kw, status):
+    assert _apply_status(ad=_ad(**kw)) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(ldx=200), P.PLORA_ERR_INVALID_ARG),
+    (dict(ldy=100), P.PLORA_ERR_INVALID_ARG),
+    (dict(ldx=260), P.PLORA_ERR_UNSUPPORTED),
+    (dict(x=None), P.PLORA_ERR_INVALID_ARG),
+    (dict(y=FAKE + 8), P.PLORA_ERR_UNSUPPORTED),
+])
+def test_operand_checks(kw, status):
+    assert _apply_status(**kw) == status
+
+
+def test_segment_struct_checks():
+    assert _apply_status(seg=_seg(cap=3)) == P.PLORA_ERR_INVALID_ARG
+    assert _apply_status(seg=_seg(tile_cap=99)) == P.PLORA_ERR_INVALID_ARG
+    assert _apply_status(seg=_seg(T=-1, cap=-1, tile_cap=0)) == P.PLORA_ERR_INVALID_ARG
+    big = P.PLORA_MAX_TOKENS + 1
+    assert _apply_status(seg=_seg(T=big, N=4)) == P.PLORA_ERR_UNSUPPORTED
+    assert _apply_status(seg=_seg(perm=None)) == P.PLORA_ERR_INVALID_ARG
+
+
+def test_empty_batch_is_a_no_op_everywhere():
+    ad = _ad()
+    seg = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    assert P.lib.plora_segment(None, ctypes.byref(seg), 4, None, 0, None) == P.PLORA_OK
+    assert _apply_status(seg=seg, x=None, y=None) == P.PLORA_OK
+    assert P.lib.plora_expand(None, 8, ctypes.byref(ad), ctypes.byref(seg), None, 256,
+                              None, 0, None) == P.PLORA_OK
+    ws = P.plora_workspace_bytes(0, ad)
+    assert P.lib.plora_shrink(None, 256, ctypes.byref(ad), ctypes.byref(seg), None, 8,
+                              FAKE, ws, None) == P.PLORA_OK
+
+
+def test_segment_rejects_oversized_key_space():
+    # 2^ceil(log2 T) * (N + 1) must fit 32 bits
+    T = 16384
+    N = 1 << 20
+    seg = _seg(T=T, N=N)
+    assert P.lib.plora_segment(FAKE, ctypes.byref(seg), N, None, 0, None) == \
+        P.PLORA_ERR_UNSUPPORTED
+
+
+def test_shrink_and_expand_leading_dimension_checks():
+    ad, seg = _ad(), _seg()
+    ws = P.plora_workspace_bytes(8, ad)
+    st = P.lib.plora_shrink(FAKE, 256, ctypes.byref(ad), ctypes.byref(seg), FAKE, 4,
+                            FAKE, ws, None)
+    assert st == P.PLORA_ERR_INVALID_ARG  # ldv < max_rank
+    st = P.lib.plora_shrink(FAKE, 256, ctypes.byref(ad), ctypes.byref(seg), FAKE, 10,
+                            FAKE, ws, None)
+    assert st == P.PLORA_ERR_UNSUPPORTED  # ldv not a multiple of 4
+    st = P.lib.plora_expand(FAKE, 8, ctypes.byref(ad), ctypes.byref(seg), FAKE, 255,
+                            None, 0, None)
+    assert st == P.PLORA_ERR_INVALID_ARG
