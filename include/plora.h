@@ -54,7 +54,9 @@
  *                              T above PLORA_MAX_TOKENS; (N+1) * 2^ceil(log2 T)
  *                              beyond 2^32
  *   PLORA_ERR_WORKSPACE_TOO_SMALL  ws_bytes below plora_workspace_bytes()
- *   PLORA_ERR_HIP              a launch failed (hipGetLastError)
+ *   PLORA_ERR_HIP              this call's launch failed (hipGetLastError;
+ *                              an error left pending by earlier HIP calls
+ *                              is cleared before launching)
  * T == 0 launches nothing, writes nothing and returns PLORA_OK.
  * Conditions only the device can see never trap: a token whose idx is -1
  * (no adapter) or outside [0, N) keeps y_base and is counted in meta; an
@@ -229,6 +231,9 @@ const char* plora_status_string(plora_status status);
  * work groups took that path, from a workspace (synchronous copy).
  */
 void plora_debug_set_spin_limit(int32_t polls);
+/* The hipError_t of the most recent launch that returned PLORA_ERR_HIP, 0 if
+ * none did. */
+int32_t plora_debug_last_hip_error(void);
 int64_t plora_debug_fallbacks(const void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus

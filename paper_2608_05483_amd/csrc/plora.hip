@@ -35,7 +35,6 @@
 
 #include <algorithm>
 #include <atomic>
-#include <mutex>
 
 #include "plora.h"
 
@@ -113,14 +112,15 @@ __device__ int block_exscan(int v, int* total, int* sh /* [kSegWaves + 1] */) {
 }
 
 // Words are (key << tbits) | t, key = adapter id or N for skipped tokens.
-// Dynamic LDS: two word buffers of T entries each.
 __global__ __launch_bounds__(kSegThreads) void segment_kernel(
     const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t cap,
     int32_t tile_cap, int32_t tbits, int32_t key_bits,
     int32_t* __restrict__ perm, int32_t* __restrict__ seg_ptr,
     int32_t* __restrict__ seg_id, int32_t* __restrict__ meta,
     int4* __restrict__ tiles) {
-  extern __shared__ uint32_t seg_lds[];
+  // Two word buffers of up to PLORA_MAX_TOKENS + 1 entries (128 KB) plus the
+  // per-wave digit cursors: static, gfx950 has 160 KB of LDS per CU.
+  __shared__ uint32_t seg_lds[2 * (PLORA_MAX_TOKENS + 1)];
   __shared__ int32_t cursor[kSegWaves][256];
   __shared__ int32_t scan_sh[kSegWaves + 1];
   __shared__ int32_t n_none_sh, n_invalid_sh;
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   n_seg = min(n_seg, cap);
   if (tid == 0) seg_lds_ptr[n_seg] = n_valid;
   __syncthreads();
-  for (int s = n_seg + 1 + tid; s <= cap; s += kSegThreads) seg_ptr[s] = n_valid;
+  for (int s = n_seg + tid; s <= cap; s += kSegThreads) seg_ptr[s] = n_valid;
   for (int s = n_seg + tid; s < cap; s += kSegThreads) seg_id[s] = -1;
 
   // tiles: a position starts a tile when it lies a multiple of kTT past its
@@ -826,8 +826,17 @@ plora_status check_segments_host(const plora_segments* seg, int32_t N) {
   return PLORA_OK;
 }
 
+// The status of a call reports its own launch: an error left pending by
+// earlier HIP calls of the caller is cleared before launching.
+void clear_stale_error() { (void)hipGetLastError(); }
+
+std::atomic<int32_t> g_last_hip_error{0};
+
 plora_status launch_status() {
-  return hipGetLastError() == hipSuccess ? PLORA_OK : PLORA_ERR_HIP;
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return PLORA_OK;
+  g_last_hip_error.store((int32_t)e);
+  return PLORA_ERR_HIP;
 }
 
 plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* ws,
@@ -891,6 +900,7 @@ plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream)
   const size_t n16 = ws_bytes / 16;
   if (n16 == 0) return PLORA_OK;
   const unsigned blocks = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
+  clear_stale_error();
   hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, stream,
                      reinterpret_cast<uint4*>(ws), n16);
   return launch_status();
@@ -908,14 +918,8 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg, int32_
   const int tbits = ceil_log2(T);
   const int key_bits = n_adapters > 0 ? 32 - __builtin_clz((unsigned)n_adapters) : 0;
   if (tbits + key_bits > 32) return PLORA_ERR_UNSUPPORTED;
-  const size_t lds = 2 * sizeof(uint32_t) * (size_t)(T + 1);
-  static std::once_flag once;
-  std::call_once(once, [] {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(segment_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                              2 * sizeof(uint32_t) * (PLORA_MAX_TOKENS + 1));
-  });
-  hipLaunchKernelGGL(segment_kernel, dim3(1), dim3(kSegThreads), lds, stream, idx, T,
+  clear_stale_error();
+  hipLaunchKernelGGL(segment_kernel, dim3(1), dim3(kSegThreads), 0, stream, idx, T,
                      n_adapters, seg->cap, seg->tile_cap, tbits, key_bits, seg->perm,
                      seg->seg_ptr, seg->seg_id, seg->meta,
                      reinterpret_cast<int4*>(seg->tiles));
@@ -933,6 +937,7 @@ plora_status plora_shrink(const uint16_t* x, int64_t ldx, const plora_adapters* 
   if (ldx < ad->h_in || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldv & 3) || !aligned16(x) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.v = v; g.ldv = ldv;
+  clear_stale_error();
   hipLaunchKernelGGL(shrink_kernel, dim3(grid_for(g)), dim3(kWave),
                      smem_bytes(g.rows_max, g.max_rank), stream, g);
   return launch_status();
@@ -949,6 +954,7 @@ plora_status plora_expand(const float* v, int64_t ldv, const plora_adapters* ad,
   if (ldy < ad->h_out || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldy & 7) || (ldv & 3) || !aligned16(y) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.v = const_cast<float*>(v); g.ldv = ldv; g.y = y; g.ldy = ldy;
+  clear_stale_error();
   hipLaunchKernelGGL(expand_kernel, dim3(grid_for(g)), dim3(kWave),
                      smem_bytes(g.rows_max, g.max_rank), stream, g);
   return launch_status();
@@ -965,6 +971,7 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
+  clear_stale_error();
   hipLaunchKernelGGL(apply_kernel, dim3(grid_for(g)), dim3(kWave),
                      smem_bytes(g.rows_max, g.max_rank), stream, g);
   return launch_status();
@@ -1024,6 +1031,8 @@ const char* plora_status_string(plora_status status) {
 void plora_debug_set_spin_limit(int32_t polls) {
   g_spin_limit.store(polls > 0 ? polls : kDefaultSpin);
 }
+
+int32_t plora_debug_last_hip_error(void) { return g_last_hip_error.load(); }
 
 int64_t plora_debug_fallbacks(const void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!ws || ws_bytes < 256) return -1;

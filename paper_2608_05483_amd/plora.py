@@ -29,12 +29,16 @@ PLORA_META_WORDS = 8
 EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
             "plora_check_adapters", "plora_status_string",
-            "plora_debug_set_spin_limit", "plora_debug_fallbacks")
+            "plora_debug_set_spin_limit", "plora_debug_fallbacks",
+            "plora_debug_last_hip_error")
 
 
 class PloraError(RuntimeError):
     def __init__(self, fn: str, status: int):
-        super().__init__(f"{fn}: {status_string(status)}")
+        msg = f"{fn}: {status_string(status)}"
+        if status == PLORA_ERR_HIP:
+            msg += f" (hipError_t {int(lib.plora_debug_last_hip_error())})"
+        super().__init__(msg)
         self.status = status
 
 
@@ -59,6 +63,12 @@ def _load() -> ctypes.CDLL:
     if not os.path.exists(_build.LIB):
         raise ImportError(
             f"{_build.LIB} is not built; run `python -m paper_2608_05483_amd.build`")
+    # torch ships its own libamdhip64 whose dependants name it without the
+    # ".7" suffix; if this library (linked against the system runtime) were
+    # loaded first, the process would end up with two HIP runtimes and torch's
+    # streams and allocations would be foreign to our launches.  Loading torch
+    # first makes the dynamic linker bind libplora.so to torch's runtime.
+    import torch  # noqa: F401
     L = ctypes.CDLL(_build.LIB)
     P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     AD, SG = ctypes.POINTER(plora_adapters), ctypes.POINTER(plora_segments)
@@ -76,6 +86,8 @@ def _load() -> ctypes.CDLL:
     L.plora_status_string.restype = ctypes.c_char_p
     L.plora_debug_set_spin_limit.argtypes = [i32]
     L.plora_debug_set_spin_limit.restype = None
+    L.plora_debug_last_hip_error.argtypes = []
+    L.plora_debug_last_hip_error.restype = i32
     L.plora_debug_fallbacks.argtypes = [P, sz, P]
     L.plora_debug_fallbacks.restype = i64
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",

@@ -154,3 +154,19 @@ def test_shrink_and_expand_leading_dimension_checks():
     st = P.lib.plora_expand(FAKE, 8, ctypes.byref(ad), ctypes.byref(seg), FAKE, 255,
                             None, 0, None)
     assert st == P.PLORA_ERR_INVALID_ARG
+
+
+def test_one_hip_runtime_per_process():
+    """The binding must bind libplora.so to torch's HIP runtime; a second
+    libamdhip64 in the process makes torch's streams foreign to our launches.
+    Checked in a fresh interpreter so import order is the binding's own."""
+    import subprocess
+    import sys
+    code = ("from paper_2608_05483_amd import plora\n"
+            "m = open('/proc/self/maps').read().splitlines()\n"
+            "print(len({l.split()[-1] for l in m if 'libamdhip64' in l}))\n")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True,
+                         text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip().splitlines()[-1] == "1"

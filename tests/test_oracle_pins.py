@@ -25,6 +25,7 @@ import numpy as np
 import pytest
 
 import oracle
+import refs
 from paper_2608_05483_amd import workloads as W
 
 U = 2.0 ** -24  # unit roundoff of fp32
@@ -308,33 +309,7 @@ def test_apply_closed_form_selection_adapters():
         assert (yref[t] == want).all()
 
 
-def _f64_reference(w, tokens):
-    """float64 dense y for the given tokens, and a rigorous bound on the
-    oracle's fp32 error for each element."""
-    dec = lambda b: (np.asarray(b, np.uint32) << 16).view(np.float32).astype(np.float64)
-    ys, bounds = [], []
-    for t in tokens:
-        i = int(w.idx[t])
-        yb = dec(w.y_base[t])
-        if not 0 <= i < w.n_adapters or w.ranks[i] == 0:
-            ys.append(yb)
-            bounds.append(np.zeros_like(yb))
-            continue
-        r = int(w.ranks[i])
-        Ai = dec(w.A[w.a_off[i]:w.a_off[i] + w.h_in * r]).reshape(w.h_in, r)
-        Bi = dec(w.B[w.b_off[i]:w.b_off[i] + r * w.h_out]).reshape(r, w.h_out)
-        x = dec(w.x[t])
-        s = float(w.scales[i])
-        v = x @ Ai
-        S = np.abs(x) @ np.abs(Ai)
-        d = v @ Bi
-        y = yb + s * d
-        bound = (gamma(w.h_in + r + 2) *
-                 (abs(s) * ((S + np.abs(v)) @ np.abs(Bi)) + np.abs(yb) +
-                  abs(s) * np.abs(d))) * 1.01 + 1e-300
-        ys.append(y)
-        bounds.append(bound)
-    return np.array(ys), np.array(bounds)
+_f64_reference = refs.f64_reference
 
 
 @pytest.mark.parametrize("name,scale", [("tiny", "paper"), ("tiny", "parity"),
