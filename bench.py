@@ -141,7 +141,6 @@ def main():
     apply_s = apply_ms.sum() / 1e3
     achieved = bytes_total / apply_s / 1e9
     adapter_gbps = bytes_adapter / apply_s / 1e9
-    fallbacks = ws.fallbacks()
 
     # ---- same-footprint plain-read ceiling -------------------------------------
     ceiling = None
@@ -223,7 +222,6 @@ def main():
                              round(float(np.percentile(apply_ms, 90)) * 1e3, 3)],
         "bytes_per_launch": int(bytes_total / K),
         "adapter_bytes_per_launch": int(bytes_adapter / K),
-        "fallbacks": int(fallbacks),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},

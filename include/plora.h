@@ -22,7 +22,7 @@
  *   plora_segment  group tokens by adapter id (stable counting sort)
  *   plora_shrink   v[t, :] = x[t, :] A_i            (E4's m = xA, fp32)
  *   plora_expand   y[t, :] += s_i v[t, :] B_i        (E4's y = mB)
- *   plora_apply    both in one launch; v never leaves the chip's caches
+ *   plora_apply    both in one launch; v never leaves the work group's LDS
  *
  * Data types and layouts (all row-major, element strides):
  *   x       bf16 [T, ldx], first h_in columns used
@@ -54,6 +54,7 @@
  *                              T above PLORA_MAX_TOKENS; (N+1) * 2^ceil(log2 T)
  *                              beyond 2^32
  *   PLORA_ERR_WORKSPACE_TOO_SMALL  ws_bytes below plora_workspace_bytes()
+ *                              (never, while that returns 0)
  *   PLORA_ERR_HIP              this call's launch failed (hipGetLastError;
  *                              an error left pending by earlier HIP calls
  *                              is cleared before launching)
@@ -61,8 +62,8 @@
  * Conditions only the device can see never trap: a token whose idx is -1
  * (no adapter) or outside [0, N) keeps y_base and is counted in meta; an
  * adapter whose rank is 0 is a no-op; an adapter whose rank is not a
- * multiple of 8, exceeds max_rank, or whose A_i/B_i block is misaligned or
- * runs past a_len/b_len is skipped (its tokens keep y_base) --
+ * power of two in 8..max_rank, or whose A_i/B_i block is misaligned or runs
+ * past a_len/b_len is skipped (its tokens keep y_base) --
  * plora_check_adapters reports such entries on the host.
  * Calls that share a workspace or a segments struct must not overlap in time
  * (same stream, or externally ordered).
@@ -104,11 +105,13 @@ typedef enum {
  *               sizes the workspace and the v stride
  *   A, B        flat bf16 stacks of a_len and b_len elements
  *   a_off,b_off int64 [N] element offsets of A_i and B_i (multiples of 8)
- *   ranks       int32 [N], r_i in {0, 8, 16, ..., max_rank}
+ *   ranks       int32 [N], r_i in {0, 8, 16, 32, 64, 128}, r_i <= max_rank
  *   scales      fp32  [N], s_i
- * Ranks that are not multiples of 8 are not supported: an adapter of rank
- * r < 8k is stored with its A_i columns and B_i rows zero-padded to the next
- * multiple of 8, which leaves every result unchanged.
+ * Other ranks (the paper's range is 2..128 and its evaluation draws from
+ * {8, 16, 32, 64, 128}) are stored zero-padded to the next of these sizes:
+ * zero columns of A_i and zero rows of B_i leave every result unchanged.
+ * h_in is limited by LDS: 8 h_in + 128 max_rank + 128 bytes <= 160 KiB
+ * (h_in up to 16384 at max_rank 128); larger shapes are UNSUPPORTED.
  */
 typedef struct {
   int32_t n_adapters;
@@ -162,13 +165,13 @@ typedef struct {
  * tiles a batch of T tokens over N adapters can produce; 0 for T <= 0. */
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 
-/* Host.  Bytes of device workspace plora_shrink / plora_apply need for a
- * batch of T tokens over this adapter stack (only the host scalars of *ad are
- * read).  plora_segment and plora_expand need none. */
+/* Host.  Bytes of device workspace the calls need for a batch of T tokens
+ * over this adapter stack.  Every kernel of this version keeps its
+ * intermediates in LDS, so this returns 0 and ws may be NULL everywhere; the
+ * arguments stay in the ABI so that a later version can ask for scratch. */
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad);
 
-/* Zero a workspace before its first use (it is left zeroed by every call
- * afterwards, so this is needed once per allocation).  Enqueued on stream. */
+/* Zero a workspace (enqueued on stream; a no-op for ws_bytes == 0). */
 plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
@@ -184,7 +187,7 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg,
 /*
  * v[t, c] = sum_k x[t, k] * A_i[k, c] for every valid token t and c < r_i
  * (the rank-r reduction m = xA of strategy E4, section V-A).  Entries of v
- * for other tokens and columns are not written.  Needs the workspace.
+ * for other tokens and columns are not written.
  */
 plora_status plora_shrink(const uint16_t* x, int64_t ldx,
                           const plora_adapters* ad, const plora_segments* seg,
@@ -203,7 +206,7 @@ plora_status plora_expand(const float* v, int64_t ldv,
 /*
  * The fused apply, one launch: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for
  * every valid token (strategy E1: both matrices resident in GPU memory,
- * section V-A).  x and y must not overlap.  Needs the workspace.
+ * section V-A).  x and y must not overlap.
  */
 plora_status plora_apply(const uint16_t* x, int64_t ldx,
                          const plora_adapters* ad, const plora_segments* seg,
@@ -213,7 +216,7 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx,
 /*
  * Host, synchronous (copies ranks and offsets to the host and waits on
  * stream).  Returns PLORA_OK if every adapter entry is usable by the kernels
- * (rank 0 or a multiple of 8 up to max_rank; offsets multiples of 8; blocks
+ * (rank 0 or a power of two in 8..max_rank; offsets multiples of 8; blocks
  * inside a_len / b_len), else PLORA_ERR_INVALID_ARG with the first bad
  * adapter index in *bad_index (may be NULL).  Not for the hot path.
  */
@@ -223,18 +226,9 @@ plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
 /* Static string naming a status code. */
 const char* plora_status_string(plora_status status);
 
-/*
- * Test hooks.  plora_debug_set_spin_limit sets, process-wide, how many polls
- * a fused-apply work group makes on its tile's arrival counter before it
- * stops waiting and recomputes the tile's whole x A_i itself (bitwise the
- * same result); 0 restores the default.  plora_debug_fallbacks reads how many
- * work groups took that path, from a workspace (synchronous copy).
- */
-void plora_debug_set_spin_limit(int32_t polls);
-/* The hipError_t of the most recent launch that returned PLORA_ERR_HIP, 0 if
- * none did. */
+/* Test hook: the hipError_t of the most recent launch that returned
+ * PLORA_ERR_HIP in this process, 0 if none did. */
 int32_t plora_debug_last_hip_error(void);
-int64_t plora_debug_fallbacks(const void* ws, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -5,29 +5,10 @@
 //   plora_segment  one 1024-thread work group: LSD radix sort of packed
 //                  (adapter id, token index) words in LDS, ballot-based stable
 //                  ranking per wavefront, then segment and tile lists.
-//   plora_shrink   one wavefront per (tile, part): split-K over h_in.  Each
-//   plora_expand   part streams its rows of A_i (or columns of B_i) once with
-//   plora_apply    128-bit loads; partial x A_i sums meet in the workspace.
-//
-// Work decomposition.  The token batch is grouped into segments (one per
-// adapter, section VI-B of the paper: the per-adapter batch B_i) and each
-// segment into tiles of at most PLORA_TILE_TOKENS tokens.  A tile is split
-// into Q parts: part q owns rows [k0_q, k1_q) of A_i and column octets
-// [o0_q, o1_q) of B_i, so every byte of an adapter is read by exactly one
-// work group per tile -- the "adapter loads its matrices once per step"
-// property of the cost model.  Work group b handles tile u = (b/8/Q)*8 + b%8,
-// part q = (b/8) % Q: the Q parts of a tile share b % 8 and hence (with the
-// round-robin assignment of work groups to the eight XCDs) one L2, where
-// their partial sums meet.
-//
-// Fused apply.  Every part first computes its partial P_q = x_tile A_i[k0_q:
-// k1_q, :], stores it to the workspace and bumps the tile's arrival counter;
-// its B_i columns are already in flight.  It then waits for all Q partials,
-// sums them in the fixed order q = 0..Q-1 and applies its B_i columns.  The
-// wait is bounded: after spin_limit polls the work group recomputes all Q
-// partials itself with the same code and order (bitwise the same v), so no
-// schedule can deadlock.  The last of the Q parts to finish resets the
-// tile's counters, leaving the workspace zeroed for the next call.
+//   plora_shrink   one work group per tile (PLORA_TILE_TOKENS tokens of one
+//   plora_expand   adapter, section VI-B's per-adapter batch B_i split into
+//   plora_apply    tiles), streaming that adapter's A_i and B_i once with
+//                  128-bit loads; details above the apply kernels below.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -43,13 +24,9 @@ namespace {
 constexpr int kTT = PLORA_TILE_TOKENS;   // tokens per tile
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
-constexpr int kWave = 64;                // apply work group = one wavefront
 constexpr int kTG = 4;                   // tokens per register group
 constexpr int kCH = 8;                   // 16-byte chunks per lane per batch
-constexpr int kMaxQ = 64;
-constexpr int kDefaultSpin = 1 << 16;
-
-std::atomic<int32_t> g_spin_limit{kDefaultSpin};
+constexpr size_t kMaxLds = 160 * 1024;   // LDS per CU on gfx950
 
 // ---------------------------------------------------------------------------
 // small device helpers
@@ -309,8 +286,35 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// apply kernels: shared pieces
+// apply kernels: one work group per tile
 // ---------------------------------------------------------------------------
+//
+// A work group of kNT threads owns one tile (<= PLORA_TILE_TOKENS tokens of
+// one adapter) and reads every byte of that adapter's A_i and B_i once.
+//
+// Shrink.  A_i is a contiguous block of h_in x r bf16 values, i.e. h_in * r/8
+// 16-byte chunks; thread tid loads chunks tid, tid + kNT, ... so the work
+// group streams the block front to back with 128-bit loads.  Because kNT is a
+// multiple of r/8, each thread always sees the same column octet
+// oct = tid % (r/8) and a set of rows.  For a group of kTG tokens it keeps
+// acc[token][8 columns] over its rows, then the partial sums of the threads
+// that share a column octet are combined: inside the wavefront by a butterfly
+// reduce-scatter over the lane bits that select the row (each step halves the
+// values a lane holds), across wavefronts through LDS in wave order.
+//
+// Expand.  B_i is r x h_out; thread (wave w, lane l) owns column octet
+// w * CPW + l % CPW (plus multiples of kW * CPW) and rows l / CPW + j * RSB,
+// with RSB row slots per octet chosen so that the whole work group covers
+// h_out.  Row-slot partial sums are combined by a butterfly all-reduce inside
+// the wavefront and row slot 0 writes y with one 16-byte read-modify-write
+// per token and octet.
+//
+// Every reduction has a fixed order, so results are bitwise reproducible,
+// and the split calls (plora_shrink then plora_expand) run the very same
+// code on the very same values as the fused call.
+
+constexpr int kNT = 512;             // threads per tile work group
+constexpr int kW = kNT / 64;         // wavefronts per work group
 
 struct ApplyArgs {
   const uint16_t* x;
@@ -328,36 +332,30 @@ struct ApplyArgs {
   const float* scales;
   const int32_t* perm;
   const int4* tiles;
-  int32_t* arrive;     // workspace counters [tile_cap]
-  int32_t* consume;
-  float* partial;      // workspace [Q][T][max_rank]
-  unsigned long long* stats;
-  int32_t T, N, h_in, h_out, max_rank, tile_cap, Q, rows_max, spin_limit;
+  int32_t T, N, h_in, h_out, max_rank, tile_cap;
+  int32_t rsb_log2;    // expand row slots per column octet (log2)
 };
 
 struct Tile {
-  int a, p0, L, u, q;
+  int a, p0, L;
   int r;
   const uint16_t* Ai;
   const uint16_t* Bi;
   float s;
 };
 
-// Decode work group b into its tile and part and validate the adapter.
-// Returns false when the group has nothing to do (padding, skipped adapter);
-// the decision is the same for every part of a tile.
+// Read and validate work group's tile.  Returns false (for the whole work
+// group) for padding entries and for adapters the kernels must skip.
 __device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t) {
-  const int b = blockIdx.x;
-  const int i = b >> 3;
-  t.u = (i / g.Q) * 8 + (b & 7);
-  t.q = i % g.Q;
-  if (t.u >= g.tile_cap) return false;
-  const int4 ti = g.tiles[t.u];
+  const int u = blockIdx.x;
+  if (u >= g.tile_cap) return false;
+  const int4 ti = g.tiles[u];
   t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
   if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
     return false;
   t.r = g.ranks[t.a];
-  if (t.r <= 0 || t.r > g.max_rank || (t.r & 7)) return false;
+  // ranks 8, 16, 32, 64, 128 (up to max_rank); anything else is skipped
+  if (t.r < 8 || t.r > g.max_rank || (t.r & (t.r - 1))) return false;
   const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
   if (ao < 0 || (ao & 7) || ao + (int64_t)g.h_in * t.r > g.a_len) return false;
   if (bo < 0 || (bo & 7) || bo + (int64_t)g.h_out * t.r > g.b_len) return false;
@@ -367,383 +365,284 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t) {
   return true;
 }
 
-// LDS carve-up of an apply work group.
+// LDS of a tile work group.  red (the cross-wavefront partial sums) aliases
+// the head of xs: it is only written after every wavefront has finished
+// reading xs for the current token group.
 struct Smem {
-  int* tok;        // [kTT]
-  uint16_t* xs;    // [rows_max][kTT] bf16, token fastest
-  float* red;      // [kTG * 8][kWave]
-  float* vs;       // [max_rank][kTT]
-  int* flag;       // [4]
+  int* tok;        // [kTT] token index of each tile row, -1 if unusable
+  float* vs;       // [max_rank][kTT] v of the tile, column-major
+  uint16_t* xs;    // [h_in][kTG] bf16 x of the current token group
+  float* red;      // [kW][kTG][max_rank]
 };
 
-__device__ __forceinline__ Smem carve(void* base, int rows_max, int max_rank) {
+__host__ __device__ constexpr size_t smem_bytes(int h_in, int max_rank) {
+  return kTT * sizeof(int) + (size_t)max_rank * kTT * sizeof(float) +
+         ((size_t)h_in * kTG * sizeof(uint16_t) > (size_t)kW * kTG * max_rank * sizeof(float)
+              ? (size_t)h_in * kTG * sizeof(uint16_t)
+              : (size_t)kW * kTG * max_rank * sizeof(float));
+}
+
+__device__ __forceinline__ Smem carve(void* base, int max_rank) {
   char* p = reinterpret_cast<char*>(base);
   Smem s;
-  s.tok = reinterpret_cast<int*>(p);              p += kTT * sizeof(int);
-  s.flag = reinterpret_cast<int*>(p);             p += 4 * sizeof(int);
-  s.red = reinterpret_cast<float*>(p);            p += kTG * 8 * kWave * sizeof(float);
-  s.vs = reinterpret_cast<float*>(p);             p += (size_t)max_rank * kTT * sizeof(float);
+  s.tok = reinterpret_cast<int*>(p);    p += kTT * sizeof(int);
+  s.vs = reinterpret_cast<float*>(p);   p += (size_t)max_rank * kTT * sizeof(float);
   s.xs = reinterpret_cast<uint16_t*>(p);
-  (void)rows_max;
+  s.red = reinterpret_cast<float*>(p);
   return s;
 }
 
-__host__ __device__ constexpr size_t smem_bytes(int rows_max, int max_rank) {
-  return kTT * sizeof(int) + 4 * sizeof(int) + kTG * 8 * kWave * sizeof(float) +
-         (size_t)max_rank * kTT * sizeof(float) + (size_t)rows_max * kTT * sizeof(uint16_t);
-}
-
-__device__ __forceinline__ void part_rows(int h_in, int Q, int q, int& k0, int& k1) {
-  const int n8 = h_in >> 3;
-  k0 = 8 * (int)(((int64_t)q * n8) / Q);
-  k1 = 8 * (int)(((int64_t)(q + 1) * n8) / Q);
-}
-
-__device__ __forceinline__ void part_octs(int h_out, int Q, int q, int& o0, int& o1) {
-  const int n8 = h_out >> 3;
-  o0 = (int)(((int64_t)q * n8) / Q);
-  o1 = (int)(((int64_t)(q + 1) * n8) / Q);
-}
-
-// Token rows of the tile into LDS.
 __device__ __forceinline__ void load_tokens(const ApplyArgs& g, const Tile& t, int* tok) {
-  const int lane = threadIdx.x;
-  if (lane < t.L) {
-    int tk = g.perm[t.p0 + lane];
-    tok[lane] = (tk >= 0 && tk < g.T) ? tk : -1;
+  if (threadIdx.x < kTT) {
+    int tk = -1;
+    if ((int)threadIdx.x < t.L) {
+      tk = g.perm[t.p0 + threadIdx.x];
+      if (tk < 0 || tk >= g.T) tk = -1;
+    }
+    tok[threadIdx.x] = tk;
   }
-  __syncthreads();
 }
 
-// Stage x[tok_l, k0:k1) for l < L into xs[row][l], bf16.  Invalid token rows
-// (never produced by plora_segment) read as zero.
-__device__ void stage_x(const ApplyArgs& g, const Tile& t, const int* tok, int k0,
-                        int nrows, uint16_t* xs) {
-  const int lane = threadIdx.x;
-  const int n8 = nrows >> 3;
-  const int total = t.L * n8;
-  for (int c = lane; c < total; c += kWave) {
-    const int l = c / n8, kc = c - l * n8;
-    const int tk = tok[l];
+// x rows of tokens g0..g0+kTG-1 into xs[k][tt], zero for missing tokens.
+__device__ void stage_x(const ApplyArgs& g, const int* tok, int g0, int L, uint16_t* xs) {
+  const int n8 = g.h_in >> 3;
+  const int total = kTG * n8;
+  for (int c = threadIdx.x; c < total; c += kNT) {
+    const int tt = c / n8, kc = c - tt * n8;
+    const int l = g0 + tt;
+    const int tk = l < L ? tok[l] : -1;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (tk >= 0) v = ldg16(g.x + (int64_t)tk * g.ldx + k0 + kc * 8);
-    uint16_t* d = xs + (kc * 8) * kTT + l;
-    d[0 * kTT] = (uint16_t)(v.x & 0xffffu); d[1 * kTT] = (uint16_t)(v.x >> 16);
-    d[2 * kTT] = (uint16_t)(v.y & 0xffffu); d[3 * kTT] = (uint16_t)(v.y >> 16);
-    d[4 * kTT] = (uint16_t)(v.z & 0xffffu); d[5 * kTT] = (uint16_t)(v.z >> 16);
-    d[6 * kTT] = (uint16_t)(v.w & 0xffffu); d[7 * kTT] = (uint16_t)(v.w >> 16);
+    if (tk >= 0) v = ldg16(g.x + (int64_t)tk * g.ldx + kc * 8);
+    uint16_t* d = xs + (kc * 8) * kTG + tt;
+    d[0 * kTG] = (uint16_t)(v.x & 0xffffu); d[1 * kTG] = (uint16_t)(v.x >> 16);
+    d[2 * kTG] = (uint16_t)(v.y & 0xffffu); d[3 * kTG] = (uint16_t)(v.y >> 16);
+    d[4 * kTG] = (uint16_t)(v.z & 0xffffu); d[5 * kTG] = (uint16_t)(v.z >> 16);
+    d[6 * kTG] = (uint16_t)(v.w & 0xffffu); d[7 * kTG] = (uint16_t)(v.w >> 16);
   }
-  __syncthreads();
 }
 
-// The shrink of one part: for each token group, acc[tt][e] over this lane's
-// rows, then a fixed-order reduction across the lanes that share a column
-// octet.  Calls sink(l, c, value) for every l < L, c < r.
-template <class Sink>
-__device__ void shrink_part(const ApplyArgs& g, const Tile& t, int q, const Smem& sm,
-                            Sink sink) {
-  const int lane = threadIdx.x;
-  int k0, k1;
-  part_rows(g.h_in, g.Q, q, k0, k1);
-  const int nrows = k1 - k0;
-  const int r = t.r, r_oct = r >> 3;
-  const int RS = kWave / r_oct;
-  const int oct = lane % r_oct, rs = lane / r_oct;
-  const bool act = rs < RS;
-  const int nj = (act && nrows > rs) ? (nrows - rs + RS - 1) / RS : 0;
+// One butterfly step over lane mask M on N values: the lane whose mask bit is
+// set keeps the upper half, the other the lower half, each adding the half
+// its partner sends.
+template <int N, int M>
+__device__ __forceinline__ void halve(float (&val)[kTG * 8], int lane) {
+  const bool up = (lane & M) != 0;
+#pragma unroll
+  for (int i = 0; i < N / 2; ++i) {
+    const float lo = val[i], hi = val[i + N / 2];
+    const float send = up ? lo : hi;
+    const float keep = up ? hi : lo;
+    val[i] = keep + __shfl_xor(send, M, 64);
+  }
+}
 
-  stage_x(g, t, sm.tok, k0, nrows, sm.xs);
-
-  const uint16_t* abase = t.Ai + (int64_t)(k0 + rs) * r + oct * 8;
-  const int64_t astep = (int64_t)RS * r;
+// v[l][c] for the whole tile into sm.vs (c < r, l < L; zero elsewhere).
+template <int R_OCT>
+__device__ void shrink_tile(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  constexpr int R = 8 * R_OCT;
+  constexpr int RSW = 64 / R_OCT;          // row slots inside a wavefront
+  constexpr int HALV = RSW >= 32 ? 5 : (RSW == 16 ? 4 : (RSW == 8 ? 3 : 2));
+  constexpr int VL = (kTG * 8) >> HALV;    // values a lane keeps
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int oct = tid % R_OCT;
+  const int n_chunks = g.h_in * R_OCT;     // 16-byte chunks of A_i
+  const int nj = tid < n_chunks ? (n_chunks - tid + kNT - 1) / kNT : 0;
+  const uint16_t* ap = t.Ai + (int64_t)tid * 8;
 
   for (int g0 = 0; g0 < t.L; g0 += kTG) {
-    float acc[kTG][8];
+    stage_x(g, sm.tok, g0, t.L, sm.xs);
+    __syncthreads();
+    float val[kTG * 8];
 #pragma unroll
-    for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[tt][e] = 0.f;
-
+    for (int i = 0; i < kTG * 8; ++i) val[i] = 0.f;
     for (int jb = 0; jb < nj; jb += kCH) {
       uint4 a[kCH];
 #pragma unroll
       for (int j = 0; j < kCH; ++j)
-        a[j] = (jb + j < nj) ? ldg16(abase + (jb + j) * astep) : make_uint4(0, 0, 0, 0);
+        a[j] = (jb + j < nj) ? ldg16(ap + (int64_t)(jb + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
 #pragma unroll
       for (int j = 0; j < kCH; ++j) {
         if (jb + j < nj) {
-          const int row = rs + (jb + j) * RS;
-          const uint2 xv = *reinterpret_cast<const uint2*>(sm.xs + row * kTT + g0);
-          float xf[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
+          const int row = (tid + (jb + j) * kNT) / R_OCT;
+          const uint2 xv = *reinterpret_cast<const uint2*>(sm.xs + row * kTG);
+          const float xf[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
           float af[8];
           unpack8(a[j], af);
 #pragma unroll
           for (int tt = 0; tt < kTG; ++tt)
 #pragma unroll
-            for (int e = 0; e < 8; ++e) acc[tt][e] = fmaf(xf[tt], af[e], acc[tt][e]);
+            for (int e = 0; e < 8; ++e) val[tt * 8 + e] = fmaf(xf[tt], af[e], val[tt * 8 + e]);
         }
       }
     }
-    // cross-lane reduction through LDS: red[(tt*8+e)][lane]
+    // reduce-scatter across the row slots of the wavefront
+    int base = 0;
+    if constexpr (HALV >= 1) { halve<32, R_OCT * 1>(val, lane); base += (lane & (R_OCT * 1)) ? 16 : 0; }
+    if constexpr (HALV >= 2) { halve<16, R_OCT * 2>(val, lane); base += (lane & (R_OCT * 2)) ? 8 : 0; }
+    if constexpr (HALV >= 3) { halve<8, R_OCT * 4>(val, lane); base += (lane & (R_OCT * 4)) ? 4 : 0; }
+    if constexpr (HALV >= 4) { halve<4, R_OCT * 8>(val, lane); base += (lane & (R_OCT * 8)) ? 2 : 0; }
+    if constexpr (HALV >= 5) { halve<2, R_OCT * 16>(val, lane); base += (lane & (R_OCT * 16)) ? 1 : 0; }
+    bool writer = true;
+    if constexpr (RSW == 64) {             // r = 8: one more all-reduce step
+      val[0] += __shfl_xor(val[0], 32, 64);
+      writer = (lane & 32) == 0;
+    }
+    __syncthreads();                        // xs is dead; red may overwrite it
+    if (writer) {
 #pragma unroll
-    for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) sm.red[(tt * 8 + e) * kWave + lane] = acc[tt][e];
-    __syncthreads();
-    const int gl = min(kTG, t.L - g0);
-    const int nout = gl * r;
-    for (int o = lane; o < nout; o += kWave) {
-      const int tt = o / r, c = o - tt * r;
-      const int oc = c >> 3, e = c & 7;
-      const float* src = sm.red + (tt * 8 + e) * kWave + oc;
-      float s = 0.f;
-      for (int k = 0; k < RS; ++k) s += src[k * r_oct];
-      sink(g0 + tt, c, s);
+      for (int j = 0; j < VL; ++j) {
+        const int idx = base + j;
+        const int tt = idx >> 3, e = idx & 7;
+        sm.red[(w * kTG + tt) * R + oct * 8 + e] = val[j];
+      }
     }
     __syncthreads();
+    for (int o = tid; o < kTG * R; o += kNT) {
+      const int tt = o / R, c = o - tt * R;
+      if (g0 + tt < t.L) {
+        float s = sm.red[tt * R + c];
+#pragma unroll
+        for (int ww = 1; ww < kW; ++ww) s += sm.red[(ww * kTG + tt) * R + c];
+        sm.vs[c * kTT + g0 + tt] = s;
+      }
+    }
+    __syncthreads();                        // red/xs free for the next group
   }
 }
 
-// The expand of one part for every token of the tile: columns octets
-// [o0, o1) of y, d = v B_i[:, cols], y = bf16(y + s d).
-__device__ void expand_part(const ApplyArgs& g, const Tile& t, int q, const Smem& sm,
-                            const uint4* bpre, int npre) {
-  const int lane = threadIdx.x;
-  int o0, o1;
-  part_octs(g.h_out, g.Q, q, o0, o1);
-  const int n_co = o1 - o0;
+__device__ __forceinline__ void shrink_dispatch(const ApplyArgs& g, const Tile& t,
+                                                const Smem& sm) {
+  switch (t.r >> 3) {
+    case 1: shrink_tile<1>(g, t, sm); break;
+    case 2: shrink_tile<2>(g, t, sm); break;
+    case 4: shrink_tile<4>(g, t, sm); break;
+    case 8: shrink_tile<8>(g, t, sm); break;
+    case 16: shrink_tile<16>(g, t, sm); break;
+    default: break;  // excluded by load_tile
+  }
+}
+
+// y[tok, cols] = bf16(y + s * v B_i[:, cols]) for every token of the tile.
+__device__ void expand_tile(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int RSB = 1 << g.rsb_log2;
+  const int CPW = 64 / RSB;                  // column octets per wavefront
+  const int n_oct = g.h_out >> 3;
+  const int co_l = lane % CPW, rb = lane / CPW;
   const int r = t.r;
-  for (int cb = 0; cb * kWave < n_co; ++cb) {
-    const int cw = min(kWave, n_co - cb * kWave);
-    const int RSB = kWave / cw;
-    const int col = lane % cw, rsb = lane / cw;
-    const bool act = rsb < RSB;
-    const int njb = (act && r > rsb) ? (r - rsb + RSB - 1) / RSB : 0;
-    const uint16_t* bbase = t.Bi + (int64_t)rsb * g.h_out + (int64_t)(o0 + cb * kWave + col) * 8;
+  const int njb = rb < r ? (r - rb + RSB - 1) / RSB : 0;
+  for (int co = w * CPW + co_l, cb = 0; cb * kW * CPW < n_oct; ++cb, co += kW * CPW) {
+    const bool col_ok = co < n_oct;
+    const uint16_t* bp = t.Bi + (int64_t)rb * g.h_out + (int64_t)co * 8;
     const int64_t bstep = (int64_t)RSB * g.h_out;
     for (int g0 = 0; g0 < t.L; g0 += kTG) {
-      float d[kTG][8];
+      float d[kTG * 8];
 #pragma unroll
-      for (int tt = 0; tt < kTG; ++tt)
+      for (int i = 0; i < kTG * 8; ++i) d[i] = 0.f;
+      if (col_ok) {
+        for (int jb = 0; jb < njb; jb += kCH) {
+          uint4 b[kCH];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) d[tt][e] = 0.f;
-      for (int jb = 0; jb < njb; jb += kCH) {
-        uint4 b[kCH];
-        const bool use_pre = (cb == 0 && g0 == 0 && jb == 0);
+          for (int j = 0; j < kCH; ++j)
+            b[j] = (jb + j < njb) ? ldg16(bp + (int64_t)(jb + j) * bstep) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-        for (int j = 0; j < kCH; ++j) {
-          if (use_pre && j < npre) b[j] = bpre[j];
-          else b[j] = (jb + j < njb) ? ldg16(bbase + (jb + j) * bstep) : make_uint4(0, 0, 0, 0);
-        }
+          for (int j = 0; j < kCH; ++j) {
+            if (jb + j < njb) {
+              const int c = rb + (jb + j) * RSB;
+              const float4 vv = *reinterpret_cast<const float4*>(sm.vs + c * kTT + g0);
+              const float vf[4] = {vv.x, vv.y, vv.z, vv.w};
+              float bf[8];
+              unpack8(b[j], bf);
 #pragma unroll
-        for (int j = 0; j < kCH; ++j) {
-          if (jb + j < njb) {
-            const int c = rsb + (jb + j) * RSB;
-            const float4 vv = *reinterpret_cast<const float4*>(sm.vs + c * kTT + g0);
-            const float vf[4] = {vv.x, vv.y, vv.z, vv.w};
-            float bf[8];
-            unpack8(b[j], bf);
+              for (int tt = 0; tt < kTG; ++tt)
 #pragma unroll
-            for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-              for (int e = 0; e < 8; ++e) d[tt][e] = fmaf(vf[tt], bf[e], d[tt][e]);
+                for (int e = 0; e < 8; ++e) d[tt * 8 + e] = fmaf(vf[tt], bf[e], d[tt * 8 + e]);
+            }
           }
         }
       }
+      // all-reduce across the row slots of each column octet
+      for (int m = CPW; m < 64; m <<= 1) {
 #pragma unroll
-      for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sm.red[(tt * 8 + e) * kWave + lane] = d[tt][e];
-      __syncthreads();
-      const int gl = min(kTG, t.L - g0);
-      const int nout = gl * cw;
-      for (int o = lane; o < nout; o += kWave) {
-        const int tt = o / cw, cc = o - tt * cw;
-        const int tk = sm.tok[g0 + tt];
-        if (tk < 0) continue;
-        float acc[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float* src = sm.red + (tt * 8 + e) * kWave + cc;
-          float s = 0.f;
-          for (int k = 0; k < RSB; ++k) s += src[k * cw];
-          acc[e] = s;
-        }
-        uint16_t* yp = g.y + (int64_t)tk * g.ldy + (int64_t)(o0 + cb * kWave + cc) * 8;
-        const uint4 yv = ldg16(yp);
-        float yf[8];
-        unpack8(yv, yf);
-        uint32_t ob[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, acc[e], yf[e]));
-        uint4 out;
-        out.x = ob[0] | (ob[1] << 16);
-        out.y = ob[2] | (ob[3] << 16);
-        out.z = ob[4] | (ob[5] << 16);
-        out.w = ob[6] | (ob[7] << 16);
-        *reinterpret_cast<uint4*>(yp) = out;
+        for (int i = 0; i < kTG * 8; ++i) d[i] += __shfl_xor(d[i], m, 64);
       }
-      __syncthreads();
+      if (col_ok && rb == 0) {
+#pragma unroll
+        for (int tt = 0; tt < kTG; ++tt) {
+          if (g0 + tt < t.L) {
+            const int tk = sm.tok[g0 + tt];
+            if (tk >= 0) {
+              uint16_t* yp = g.y + (int64_t)tk * g.ldy + (int64_t)co * 8;
+              const uint4 yv = ldg16(yp);
+              float yf[8];
+              unpack8(yv, yf);
+              uint32_t ob[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[tt * 8 + e], yf[e]));
+              uint4 out;
+              out.x = ob[0] | (ob[1] << 16);
+              out.y = ob[2] | (ob[3] << 16);
+              out.z = ob[4] | (ob[5] << 16);
+              out.w = ob[6] | (ob[7] << 16);
+              *reinterpret_cast<uint4*>(yp) = out;
+            }
+          }
+        }
+      }
     }
   }
 }
 
-// Issue the first batch of this part's B_i loads (rows of the first column
-// batch) so they are in flight during the shrink.
-__device__ __forceinline__ int prefetch_b(const ApplyArgs& g, const Tile& t, int q,
-                                          uint4* bpre) {
-  const int lane = threadIdx.x;
-  int o0, o1;
-  part_octs(g.h_out, g.Q, q, o0, o1);
-  const int n_co = o1 - o0;
-  if (n_co <= 0) return 0;
-  const int cw = min(kWave, n_co);
-  const int RSB = kWave / cw;
-  const int col = lane % cw, rsb = lane / cw;
-  const bool act = rsb < RSB;
-  const int njb = (act && t.r > rsb) ? (t.r - rsb + RSB - 1) / RSB : 0;
-  const uint16_t* bbase = t.Bi + (int64_t)rsb * g.h_out + (int64_t)(o0 + col) * 8;
-  const int64_t bstep = (int64_t)RSB * g.h_out;
-#pragma unroll
-  for (int j = 0; j < kCH; ++j)
-    bpre[j] = (j < njb) ? ldg16(bbase + j * bstep) : make_uint4(0, 0, 0, 0);
-  return kCH;
+// Common prologue: tile, tokens, zeroed v.  Returns false if the work group
+// has nothing to do.
+__device__ __forceinline__ bool tile_prologue(const ApplyArgs& g, Tile& t, Smem& sm,
+                                              void* lds) {
+  if (!load_tile(g, t)) return false;
+  sm = carve(lds, g.max_rank);
+  load_tokens(g, t, sm.tok);
+  for (int o = threadIdx.x; o < g.max_rank * kTT; o += kNT) sm.vs[o] = 0.f;
+  __syncthreads();
+  return true;
 }
 
 // ---------------------------------------------------------------------------
 // kernels
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kWave) void shrink_kernel(ApplyArgs g) {
+__global__ __launch_bounds__(kNT) void shrink_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   Tile t;
-  if (!load_tile(g, t)) return;
-  const Smem sm = carve(apply_lds, g.rows_max, g.max_rank);
-  load_tokens(g, t, sm.tok);
-  float* part = g.partial + (int64_t)t.q * g.T * g.max_rank;
-  shrink_part(g, t, t.q, sm, [&](int l, int c, float val) {
-    part[(int64_t)(t.p0 + l) * g.max_rank + c] = val;
-  });
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int old = __hip_atomic_fetch_add(&g.arrive[t.u], 1, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-    sm.flag[0] = (old == g.Q - 1);
-  }
-  __syncthreads();
-  if (!sm.flag[0]) return;
-  // last part to arrive: v = sum of the Q partials in order q = 0..Q-1
-  __threadfence();
-  const int nout = t.L * t.r;
-  for (int o = threadIdx.x; o < nout; o += kWave) {
-    const int l = o / t.r, c = o - l * t.r;
-    const int64_t row = (int64_t)(t.p0 + l) * g.max_rank + c;
-    float s = __hip_atomic_load(&g.partial[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    for (int qq = 1; qq < g.Q; ++qq)
-      s += __hip_atomic_load(&g.partial[(int64_t)qq * g.T * g.max_rank + row],
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int tk = sm.tok[l];
-    if (tk >= 0) g.v[(int64_t)tk * g.ldv + c] = s;
-  }
-  if (threadIdx.x == 0)
-    __hip_atomic_store(&g.arrive[t.u], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__global__ __launch_bounds__(kWave) void expand_kernel(ApplyArgs g) {
-  extern __shared__ __align__(16) unsigned char apply_lds[];
-  Tile t;
-  if (!load_tile(g, t)) return;
-  const Smem sm = carve(apply_lds, g.rows_max, g.max_rank);
-  load_tokens(g, t, sm.tok);
-  uint4 bpre[kCH];
-  const int npre = prefetch_b(g, t, t.q, bpre);
-  const int nout = t.L * t.r;
-  for (int o = threadIdx.x; o < nout; o += kWave) {
+  Smem sm;
+  if (!tile_prologue(g, t, sm, apply_lds)) return;
+  shrink_dispatch(g, t, sm);
+  for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
     const int tk = sm.tok[l];
-    sm.vs[c * kTT + l] = tk >= 0 ? g.v[(int64_t)tk * g.ldv + c] : 0.f;
+    if (tk >= 0) g.v[(int64_t)tk * g.ldv + c] = sm.vs[c * kTT + l];
   }
-  // zero the unused token slots of the last register group
-  for (int o = threadIdx.x; o < t.r * kTT; o += kWave) {
-    const int l = o % kTT;
-    if (l >= t.L) sm.vs[o] = 0.f;
-  }
-  __syncthreads();
-  expand_part(g, t, t.q, sm, bpre, npre);
 }
 
-__global__ __launch_bounds__(kWave) void apply_kernel(ApplyArgs g) {
+__global__ __launch_bounds__(kNT) void expand_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   Tile t;
-  if (!load_tile(g, t)) return;
-  const Smem sm = carve(apply_lds, g.rows_max, g.max_rank);
-  load_tokens(g, t, sm.tok);
-  uint4 bpre[kCH];
-  const int npre = prefetch_b(g, t, t.q, bpre);
-
-  // 1. this part's partial x A_i, published to the workspace
-  float* part = g.partial + (int64_t)t.q * g.T * g.max_rank;
-  shrink_part(g, t, t.q, sm, [&](int l, int c, float val) {
-    part[(int64_t)(t.p0 + l) * g.max_rank + c] = val;
-  });
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __hip_atomic_fetch_add(&g.arrive[t.u], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    // 2. wait for the other parts, bounded
-    int polls = 0;
-    int seen = __hip_atomic_load(&g.arrive[t.u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    while (seen < g.Q && polls < g.spin_limit) {
-      __builtin_amdgcn_s_sleep(1);
-      seen = __hip_atomic_load(&g.arrive[t.u], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      ++polls;
-    }
-    sm.flag[0] = (seen >= g.Q);
+  Smem sm;
+  if (!tile_prologue(g, t, sm, apply_lds)) return;
+  for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
+    const int l = o / t.r, c = o - l * t.r;
+    const int tk = sm.tok[l];
+    if (tk >= 0) sm.vs[c * kTT + l] = g.v[(int64_t)tk * g.ldv + c];
   }
   __syncthreads();
-  const bool ready = sm.flag[0] != 0;
-  __threadfence();
+  expand_tile(g, t, sm);
+}
 
-  // 3. v = sum of the Q partials, q ascending
-  for (int o = threadIdx.x; o < t.r * kTT; o += kWave) sm.vs[o] = 0.f;
-  __syncthreads();
-  if (ready) {
-    const int nout = t.L * t.r;
-    for (int o = threadIdx.x; o < nout; o += kWave) {
-      const int l = o / t.r, c = o - l * t.r;
-      const int64_t row = (int64_t)(t.p0 + l) * g.max_rank + c;
-      float s = __hip_atomic_load(&g.partial[row], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      for (int qq = 1; qq < g.Q; ++qq)
-        s += __hip_atomic_load(&g.partial[(int64_t)qq * g.T * g.max_rank + row],
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      sm.vs[c * kTT + l] = s;
-    }
-  } else {
-    // bounded wait expired: recompute every part locally, same order
-    if (threadIdx.x == 0) atomicAdd(g.stats, 1ull);
-    for (int qq = 0; qq < g.Q; ++qq) {
-      shrink_part(g, t, qq, sm, [&](int l, int c, float val) {
-        float* dst = sm.vs + c * kTT + l;
-        *dst = (qq == 0) ? val : (*dst + val);
-      });
-    }
-  }
-  __syncthreads();
-
-  // 4. this part's columns of y
-  expand_part(g, t, t.q, sm, bpre, npre);
-
-  // 5. the last part out resets the tile's counters
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const int old = __hip_atomic_fetch_add(&g.consume[t.u], 1, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-    if (old == g.Q - 1) {
-      __hip_atomic_store(&g.arrive[t.u], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(&g.consume[t.u], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-  }
+__global__ __launch_bounds__(kNT) void apply_kernel(ApplyArgs g) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  Tile t;
+  Smem sm;
+  if (!tile_prologue(g, t, sm, apply_lds)) return;
+  shrink_dispatch(g, t, sm);
+  expand_tile(g, t, sm);
 }
 
 __global__ void zero_kernel(uint4* p, size_t n16) {
@@ -764,36 +663,17 @@ inline int ceil_log2(int64_t v) {
   return b;
 }
 
-// Parts per tile: split the adapter into pieces of at least ~8 KB, at most
-// 32 pieces, each part holding at least one row octet of A_i and one column
-// octet of B_i, and at most 512 rows of A_i (the LDS x tile).
-int parts_for(int h_in, int h_out, int max_rank) {
-  const int64_t bytes = 2LL * (h_in + h_out) * max_rank;
-  int q = 1;
-  while (q < 32 && bytes / (2 * q) >= 8192) q *= 2;
-  while (q < kMaxQ && (h_in / 8 + q - 1) / q > 64) q *= 2;
-  q = std::min(q, std::max(1, std::min(h_in / 8, h_out / 8)));
-  return q;
+inline bool usable_rank(int r, int max_rank) {
+  return r == 0 || (r >= 8 && r <= max_rank && (r & (r - 1)) == 0);
 }
 
-int rows_max_for(int h_in, int Q) { return 8 * ((h_in / 8 + Q - 1) / Q); }
-
-struct WsLayout {
-  size_t stats, arrive, consume, partial, total;
-};
-
-inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
-
-WsLayout ws_layout(int32_t T, int32_t N, int h_in, int h_out, int max_rank) {
-  WsLayout L;
-  const int tile_cap = plora_tile_capacity(T, N);
-  const int Q = parts_for(h_in, h_out, max_rank);
-  L.stats = 0;
-  L.arrive = 256;
-  L.consume = align256(L.arrive + sizeof(int32_t) * (size_t)std::max(tile_cap, 1));
-  L.partial = align256(L.consume + sizeof(int32_t) * (size_t)std::max(tile_cap, 1));
-  L.total = align256(L.partial + sizeof(float) * (size_t)Q * std::max(T, 1) * std::max(max_rank, 8));
-  return L;
+// Expand row slots per column octet: the largest power of two that still
+// lets one work group cover every column octet of y in a single pass.
+int rsb_log2_for(int h_out) {
+  const int n_oct = h_out / 8;
+  int l = 0;
+  while (l < 6 && (n_oct << (l + 1)) <= kNT) ++l;
+  return l;
 }
 
 plora_status check_adapters_host(const plora_adapters* ad) {
@@ -804,6 +684,7 @@ plora_status check_adapters_host(const plora_adapters* ad) {
   if ((ad->h_in & 7) || (ad->h_out & 7)) return PLORA_ERR_UNSUPPORTED;
   if (ad->max_rank == 0 || (ad->max_rank & 7) || ad->max_rank > PLORA_MAX_RANK)
     return PLORA_ERR_UNSUPPORTED;
+  if (smem_bytes(ad->h_in, ad->max_rank) > kMaxLds) return PLORA_ERR_UNSUPPORTED;
   if (ad->n_adapters > 0 &&
       (!ad->A || !ad->B || !ad->a_off || !ad->b_off || !ad->ranks || !ad->scales))
     return PLORA_ERR_INVALID_ARG;
@@ -840,7 +721,8 @@ plora_status launch_status() {
 }
 
 plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* ws,
-                     size_t ws_bytes, bool need_ws, ApplyArgs& g) {
+                     size_t ws_bytes, ApplyArgs& g) {
+  (void)ws; (void)ws_bytes;  // the tile kernels need no workspace
   plora_status st = check_adapters_host(ad);
   if (st != PLORA_OK) return st;
   st = check_segments_host(seg, ad->n_adapters);
@@ -852,26 +734,28 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   g.tiles = reinterpret_cast<const int4*>(seg->tiles);
   g.T = seg->T; g.N = ad->n_adapters; g.h_in = ad->h_in; g.h_out = ad->h_out;
   g.max_rank = ad->max_rank; g.tile_cap = seg->tile_cap;
-  g.Q = parts_for(ad->h_in, ad->h_out, ad->max_rank);
-  g.rows_max = rows_max_for(ad->h_in, g.Q);
-  g.spin_limit = g_spin_limit.load();
-  if (need_ws) {
-    if (!ws) return PLORA_ERR_INVALID_ARG;
-    if (!aligned16(ws)) return PLORA_ERR_UNSUPPORTED;
-    const WsLayout L = ws_layout(seg->T, ad->n_adapters, ad->h_in, ad->h_out, ad->max_rank);
-    if (ws_bytes < L.total) return PLORA_ERR_WORKSPACE_TOO_SMALL;
-    char* base = reinterpret_cast<char*>(ws);
-    g.stats = reinterpret_cast<unsigned long long*>(base + L.stats);
-    g.arrive = reinterpret_cast<int32_t*>(base + L.arrive);
-    g.consume = reinterpret_cast<int32_t*>(base + L.consume);
-    g.partial = reinterpret_cast<float*>(base + L.partial);
-  }
+  g.rsb_log2 = rsb_log2_for(ad->h_out);
   return PLORA_OK;
 }
 
-unsigned grid_for(const ApplyArgs& g) {
-  const int groups = (g.tile_cap + 7) / 8;
-  return (unsigned)groups * 8u * (unsigned)g.Q;
+// Dynamic LDS above 64 KB is opted into once per kernel.
+void allow_lds(const void* kernel, std::atomic<bool>& done) {
+  if (done.load()) return;
+  (void)hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLds);
+  (void)hipGetLastError();
+  done.store(true);
+}
+
+std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false};
+
+template <class K>
+plora_status launch_tiles(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
+                          hipStream_t stream) {
+  const size_t lds = smem_bytes(g.h_in, g.max_rank);
+  if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(kernel), lds_done);
+  clear_stale_error();
+  hipLaunchKernelGGL(kernel, dim3((unsigned)g.tile_cap), dim3(kNT), lds, stream, g);
+  return launch_status();
 }
 
 }  // namespace
@@ -889,16 +773,15 @@ int32_t plora_tile_capacity(int32_t T, int32_t n_adapters) {
 }
 
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad) {
-  if (!ad || T < 0) return 0;
-  return ws_layout(T, ad->n_adapters, std::max(ad->h_in, 8), std::max(ad->h_out, 8),
-                   std::max(ad->max_rank, 8)).total;
+  (void)T; (void)ad;
+  return 0;
 }
 
 plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (ws_bytes == 0) return PLORA_OK;
   if (!ws) return PLORA_ERR_INVALID_ARG;
   if (!aligned16(ws) || (ws_bytes & 15)) return PLORA_ERR_UNSUPPORTED;
   const size_t n16 = ws_bytes / 16;
-  if (n16 == 0) return PLORA_OK;
   const unsigned blocks = (unsigned)std::min<size_t>((n16 + 255) / 256, 4096);
   clear_stale_error();
   hipLaunchKernelGGL(zero_kernel, dim3(blocks), dim3(256), 0, stream,
@@ -930,51 +813,42 @@ plora_status plora_shrink(const uint16_t* x, int64_t ldx, const plora_adapters* 
                           const plora_segments* seg, float* v, int64_t ldv, void* ws,
                           size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, true, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!x || !v) return PLORA_ERR_INVALID_ARG;
   if (ldx < ad->h_in || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldv & 3) || !aligned16(x) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.v = v; g.ldv = ldv;
-  clear_stale_error();
-  hipLaunchKernelGGL(shrink_kernel, dim3(grid_for(g)), dim3(kWave),
-                     smem_bytes(g.rows_max, g.max_rank), stream, g);
-  return launch_status();
+  return launch_tiles(shrink_kernel, g_lds_shrink, g, stream);
 }
 
 plora_status plora_expand(const float* v, int64_t ldv, const plora_adapters* ad,
                           const plora_segments* seg, uint16_t* y, int64_t ldy, void* ws,
                           size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, false, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!v || !y) return PLORA_ERR_INVALID_ARG;
   if (ldy < ad->h_out || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldy & 7) || (ldv & 3) || !aligned16(y) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.v = const_cast<float*>(v); g.ldv = ldv; g.y = y; g.ldy = ldy;
-  clear_stale_error();
-  hipLaunchKernelGGL(expand_kernel, dim3(grid_for(g)), dim3(kWave),
-                     smem_bytes(g.rows_max, g.max_rank), stream, g);
-  return launch_status();
+  return launch_tiles(expand_kernel, g_lds_expand, g, stream);
 }
 
 plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* ad,
                          const plora_segments* seg, uint16_t* y, int64_t ldy, void* ws,
                          size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, true, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!x || !y) return PLORA_ERR_INVALID_ARG;
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
-  clear_stale_error();
-  hipLaunchKernelGGL(apply_kernel, dim3(grid_for(g)), dim3(kWave),
-                     smem_bytes(g.rows_max, g.max_rank), stream, g);
-  return launch_status();
+  return launch_tiles(apply_kernel, g_lds_apply, g, stream);
 }
 
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
@@ -999,7 +873,7 @@ plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
   } else {
     for (int i = 0; i < N; ++i) {
       const int r = ranks[i];
-      bool ok = r >= 0 && r <= ad->max_rank && (r & 7) == 0;
+      bool ok = usable_rank(r, ad->max_rank);
       if (ok && r > 0) {
         ok = ao[i] >= 0 && (ao[i] & 7) == 0 && ao[i] + (int64_t)ad->h_in * r <= ad->a_len &&
              bo[i] >= 0 && (bo[i] & 7) == 0 && bo[i] + (int64_t)ad->h_out * r <= ad->b_len;
@@ -1028,19 +902,6 @@ const char* plora_status_string(plora_status status) {
   return "PLORA_ERR_UNKNOWN";
 }
 
-void plora_debug_set_spin_limit(int32_t polls) {
-  g_spin_limit.store(polls > 0 ? polls : kDefaultSpin);
-}
-
 int32_t plora_debug_last_hip_error(void) { return g_last_hip_error.load(); }
-
-int64_t plora_debug_fallbacks(const void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!ws || ws_bytes < 256) return -1;
-  unsigned long long v = 0;
-  if (hipMemcpyAsync(&v, ws, sizeof v, hipMemcpyDeviceToHost, stream) != hipSuccess ||
-      hipStreamSynchronize(stream) != hipSuccess)
-    return -1;
-  return (int64_t)v;
-}
 
 }  // extern "C"

@@ -27,14 +27,28 @@ __global__ __launch_bounds__(kThreads) void read_kernel(
   const uint4* pb = reinterpret_cast<const uint4*>(B + b_off[id]);
   const int64_t a0 = na * part / kParts, a1 = na * (part + 1) / kParts;
   const int64_t b0 = nb * part / kParts, b1 = nb * (part + 1) / kParts;
+  // eight 16-byte loads in flight per lane before any is consumed
   uint32_t acc = 0;
-  for (int64_t i = a0 + threadIdx.x; i < a1; i += kThreads) {
-    const uint4 v = pa[i];
-    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  constexpr int kU = 8;
+  for (int64_t i0 = a0 + threadIdx.x; i0 < a1; i0 += kThreads * kU) {
+    uint4 v[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t i = i0 + (int64_t)j * kThreads;
+      v[j] = i < a1 ? pa[i] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   }
-  for (int64_t i = b0 + threadIdx.x; i < b1; i += kThreads) {
-    const uint4 v = pb[i];
-    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  for (int64_t i0 = b0 + threadIdx.x; i0 < b1; i0 += kThreads * kU) {
+    uint4 v[kU];
+#pragma unroll
+    for (int j = 0; j < kU; ++j) {
+      const int64_t i = i0 + (int64_t)j * kThreads;
+      v[j] = i < b1 ? pb[i] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kU; ++j) acc ^= v[j].x ^ v[j].y ^ v[j].z ^ v[j].w;
   }
   sink[blockIdx.x * kThreads + threadIdx.x] = acc;
 }

@@ -29,7 +29,6 @@ PLORA_META_WORDS = 8
 EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
             "plora_check_adapters", "plora_status_string",
-            "plora_debug_set_spin_limit", "plora_debug_fallbacks",
             "plora_debug_last_hip_error")
 
 
@@ -84,12 +83,8 @@ def _load() -> ctypes.CDLL:
     L.plora_check_adapters.argtypes = [AD, ctypes.POINTER(i32), P]
     L.plora_status_string.argtypes = [ctypes.c_int]
     L.plora_status_string.restype = ctypes.c_char_p
-    L.plora_debug_set_spin_limit.argtypes = [i32]
-    L.plora_debug_set_spin_limit.restype = None
     L.plora_debug_last_hip_error.argtypes = []
     L.plora_debug_last_hip_error.restype = i32
-    L.plora_debug_fallbacks.argtypes = [P, sz, P]
-    L.plora_debug_fallbacks.restype = i64
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
                "plora_expand", "plora_apply", "plora_check_adapters"):
         getattr(L, fn).restype = ctypes.c_int
@@ -155,14 +150,6 @@ def plora_check_adapters(ad: plora_adapters, stream: int) -> int:
         return bad.value
     _ok("plora_check_adapters", st)
     return -1
-
-
-def plora_debug_set_spin_limit(polls: int) -> None:
-    lib.plora_debug_set_spin_limit(polls)
-
-
-def plora_debug_fallbacks(ws: int, ws_bytes: int, stream: int) -> int:
-    return int(lib.plora_debug_fallbacks(ws, ws_bytes, stream))
 
 
 # ---- torch-backed buffers ----------------------------------------------------
@@ -233,20 +220,20 @@ class Segments:
 
 
 class Workspace:
-    """Zero-initialised workspace sized for (T, adapter stack)."""
+    """Zero-initialised workspace of plora_workspace_bytes(T, stack) bytes
+    (currently 0: the pointer passed is then NULL)."""
 
     def __init__(self, T: int, ad: Adapters, device="cuda", stream=None):
         import torch
         self.nbytes = plora_workspace_bytes(T, ad.struct)
-        self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
-        plora_workspace_init(self.buf.data_ptr(), self.nbytes, _stream(stream))
+        self.buf = None
+        if self.nbytes:
+            self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
+            plora_workspace_init(self.buf.data_ptr(), self.nbytes, _stream(stream))
 
     @property
-    def ptr(self) -> int:
-        return self.buf.data_ptr()
-
-    def fallbacks(self, stream=None) -> int:
-        return plora_debug_fallbacks(self.ptr, self.nbytes, _stream(stream))
+    def ptr(self) -> int | None:
+        return self.buf.data_ptr() if self.buf is not None else None
 
 
 def segment(idx, segs: Segments, stream=None) -> None:

@@ -78,12 +78,22 @@ def _apply_status(ad=None, seg=None, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
                              ws_bytes, None)
 
 
-def test_workspace_size_is_checked():
+def test_no_workspace_needed():
     ad = _ad()
-    need = P.plora_workspace_bytes(8, ad)
-    assert need > 0
-    assert _apply_status(ws_bytes=need - 1) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
-    assert _apply_status(ws=None) == P.PLORA_ERR_INVALID_ARG
+    assert P.plora_workspace_bytes(8, ad) == 0
+    assert P.lib.plora_workspace_init(None, 0, None) == P.PLORA_OK
+
+
+def test_lds_limit_is_checked():
+    # 8 h_in + 128 max_rank + 128 bytes must fit 160 KiB: the paper's largest
+    # model dimension at the largest rank passes the host checks, a larger one
+    # is refused.  An empty batch returns right after the checks, so nothing
+    # is ever launched on the fake pointers.
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    st = _apply_status(ad=_ad(h_in=16384, max_rank=128), seg=empty, ldx=16384)
+    assert st == P.PLORA_OK
+    st = _apply_status(ad=_ad(h_in=20480, max_rank=8), seg=empty, ldx=20480)
+    assert st == P.PLORA_ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -96,6 +106,7 @@ def test_workspace_size_is_checked():
     (dict(A=None), P.PLORA_ERR_INVALID_ARG),
     (dict(A=FAKE + 2), P.PLORA_ERR_UNSUPPORTED),
     (dict(n_adapters=-1), P.PLORA_ERR_INVALID_ARG),
+    (dict(h_in=20480), P.PLORA_ERR_UNSUPPORTED),
 ])
 def test_adapter_checks(kw, status):
     assert _apply_status(ad=_ad(**kw)) == status
