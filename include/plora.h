@@ -110,8 +110,6 @@ typedef enum {
  * Other ranks (the paper's range is 2..128 and its evaluation draws from
  * {8, 16, 32, 64, 128}) are stored zero-padded to the next of these sizes:
  * zero columns of A_i and zero rows of B_i leave every result unchanged.
- * h_in is limited by LDS: 8 h_in + 128 max_rank + 128 bytes <= 160 KiB
- * (h_in up to 16384 at max_rank 128); larger shapes are UNSUPPORTED.
  */
 typedef struct {
   int32_t n_adapters;

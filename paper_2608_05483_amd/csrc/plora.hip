@@ -24,7 +24,6 @@ namespace {
 constexpr int kTT = PLORA_TILE_TOKENS;   // tokens per tile
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
-constexpr int kTG = 4;                   // tokens per register group
 constexpr int kCH = 8;                   // 16-byte chunks per lane per batch
 constexpr size_t kMaxLds = 160 * 1024;   // LDS per CU on gfx950
 
@@ -290,24 +289,32 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // ---------------------------------------------------------------------------
 //
 // A work group of kNT threads owns one tile (<= PLORA_TILE_TOKENS tokens of
-// one adapter) and reads every byte of that adapter's A_i and B_i once.
+// one adapter) and reads every byte of that adapter's A_i and B_i once; there
+// is no communication between work groups.  Two code paths, chosen per tile:
 //
-// Shrink.  A_i is a contiguous block of h_in x r bf16 values, i.e. h_in * r/8
-// 16-byte chunks; thread tid loads chunks tid, tid + kNT, ... so the work
-// group streams the block front to back with 128-bit loads.  Because kNT is a
-// multiple of r/8, each thread always sees the same column octet
-// oct = tid % (r/8) and a set of rows.  For a group of kTG tokens it keeps
-// acc[token][8 columns] over its rows, then the partial sums of the threads
-// that share a column octet are combined: inside the wavefront by a butterfly
-// reduce-scatter over the lane bits that select the row (each step halves the
-// values a lane holds), across wavefronts through LDS in wave order.
+// Single-token tiles (vector ALU).  A_i, a contiguous block of h_in x r bf16
+// values, is streamed as 16-byte chunks: thread tid loads chunks tid, tid +
+// kNT, ... so it always sees the column octet tid % (r/8) and a set of rows,
+// and accumulates x[row] * A_i[row][octet] in registers.  Threads sharing an
+// octet are combined inside the wavefront by a butterfly (halving while more
+// than one value remains, then all-reducing the remaining row-slot bits) and
+// across wavefronts through LDS in wave order.  The expand gives each thread
+// one column octet of B_i and all (or a row-slot share of) its r rows.  The
+// first chunks of A_i and B_i, x and the y words are all requested before any
+// of them is needed, in the order they are consumed (the vector-memory
+// counter retires in order).
 //
-// Expand.  B_i is r x h_out; thread (wave w, lane l) owns column octet
-// w * CPW + l % CPW (plus multiples of kW * CPW) and rows l / CPW + j * RSB,
-// with RSB row slots per octet chosen so that the whole work group covers
-// h_out.  Row-slot partial sums are combined by a butterfly all-reduce inside
-// the wavefront and row slot 0 writes y with one 16-byte read-modify-write
-// per token and octet.
+// Multi-token tiles (matrix cores, v_mfma_f32_16x16x32_bf16).  The shrink
+// computes D[token][c] = sum_k x[token][k] A_i[k][c]: x rows feed the A
+// operand straight from global memory; A_i is staged in LDS in row chunks and
+// read back transposed (ds_read_b64_tr_b16) into the B operand.  Wavefronts
+// take interleaved 32-row K steps and their partial tiles are summed by a
+// fixed pairwise tree.  The expand computes D^T[j][token] =
+// sum_c B_i[c][j] v[token][c] with B_i column chunks staged in LDS and read
+// transposed into the A operand; v is split into bf16 high and low parts
+// (v = hi + lo to about 2^-17 relative) so that no intermediate is rounded
+// below fp32 accuracy.  Each lane then owns four consecutive y columns of one
+// token.
 //
 // Every reduction has a fixed order, so results are bitwise reproducible,
 // and the split calls (plora_shrink then plora_expand) run the very same
@@ -315,6 +322,16 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 
 constexpr int kNT = 512;             // threads per tile work group
 constexpr int kW = kNT / 64;         // wavefronts per work group
+constexpr int kAP = 16;              // A_i chunks per thread requested up front
+constexpr int kBP = 16;              // B_i chunks per thread requested up front
+constexpr int kXW = 8192;            // x row window staged in LDS (single-token path)
+constexpr int kChunk = 32768;        // bf16 elements per LDS staging chunk (64 KiB)
+constexpr int kRK = 32;              // MFMA K step
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 struct ApplyArgs {
   const uint16_t* x;
@@ -333,7 +350,7 @@ struct ApplyArgs {
   const int32_t* perm;
   const int4* tiles;
   int32_t T, N, h_in, h_out, max_rank, tile_cap;
-  int32_t rsb_log2;    // expand row slots per column octet (log2)
+  int32_t rsb_log2;    // single-token expand: row slots per column octet (log2)
 };
 
 struct Tile {
@@ -344,88 +361,114 @@ struct Tile {
   float s;
 };
 
-// Read and validate work group's tile.  Returns false (for the whole work
-// group) for padding entries and for adapters the kernels must skip.
-__device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t) {
+// Read and validate the work group's tile.  Returns false (for the whole
+// work group) for padding entries and for adapters the kernels must skip.
+// Threads below L also fetch their tile row's token index (-1 if unusable);
+// it is issued together with the adapter metadata so both arrive in one trip.
+__device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t, int& my_tok) {
   const int u = blockIdx.x;
   if (u >= g.tile_cap) return false;
   const int4 ti = g.tiles[u];
   t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
   if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
     return false;
+  my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
   t.r = g.ranks[t.a];
+  const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
+  t.s = g.scales[t.a];
+  if (my_tok < 0 || my_tok >= g.T) my_tok = -1;
   // ranks 8, 16, 32, 64, 128 (up to max_rank); anything else is skipped
   if (t.r < 8 || t.r > g.max_rank || (t.r & (t.r - 1))) return false;
-  const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
   if (ao < 0 || (ao & 7) || ao + (int64_t)g.h_in * t.r > g.a_len) return false;
   if (bo < 0 || (bo & 7) || bo + (int64_t)g.h_out * t.r > g.b_len) return false;
   t.Ai = g.A + ao;
   t.Bi = g.B + bo;
-  t.s = g.scales[t.a];
   return true;
 }
 
-// LDS of a tile work group.  red (the cross-wavefront partial sums) aliases
-// the head of xs: it is only written after every wavefront has finished
-// reading xs for the current token group.
+// Barrier for LDS traffic only: global loads into registers stay in flight.
+__device__ __forceinline__ void lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// LDS of a tile work group.
+//   tok   [kTT]              token index of each tile row, -1 if unusable
+//   vs    [max_rank][kTT]    v of the tile, fp32, column-major
+//   vhl   [2][kTT][RKmax]    v split into bf16 high and low parts, token-major
+//   buf   kChunk bf16        single-token path: x window and the cross-wave
+//                            partial sums; matrix path: A_i / B_i chunks and
+//                            the wave-tree partial tiles
 struct Smem {
-  int* tok;        // [kTT] token index of each tile row, -1 if unusable
-  float* vs;       // [max_rank][kTT] v of the tile, column-major
-  uint16_t* xs;    // [h_in][kTG] bf16 x of the current token group
-  float* red;      // [kW][kTG][max_rank]
+  int* tok;
+  float* vs;
+  uint16_t* vhl;
+  uint16_t* buf;
 };
+
+__host__ __device__ constexpr int rk_max(int max_rank) {
+  return max_rank < kRK ? kRK : max_rank;
+}
 
 __host__ __device__ constexpr size_t smem_bytes(int h_in, int max_rank) {
   return kTT * sizeof(int) + (size_t)max_rank * kTT * sizeof(float) +
-         ((size_t)h_in * kTG * sizeof(uint16_t) > (size_t)kW * kTG * max_rank * sizeof(float)
-              ? (size_t)h_in * kTG * sizeof(uint16_t)
-              : (size_t)kW * kTG * max_rank * sizeof(float));
+         (size_t)2 * kTT * rk_max(max_rank) * sizeof(uint16_t) +
+         (size_t)kChunk * sizeof(uint16_t) + 0 * h_in;
 }
 
 __device__ __forceinline__ Smem carve(void* base, int max_rank) {
   char* p = reinterpret_cast<char*>(base);
   Smem s;
-  s.tok = reinterpret_cast<int*>(p);    p += kTT * sizeof(int);
-  s.vs = reinterpret_cast<float*>(p);   p += (size_t)max_rank * kTT * sizeof(float);
-  s.xs = reinterpret_cast<uint16_t*>(p);
-  s.red = reinterpret_cast<float*>(p);
+  s.tok = reinterpret_cast<int*>(p);      p += kTT * sizeof(int);
+  s.vs = reinterpret_cast<float*>(p);     p += (size_t)max_rank * kTT * sizeof(float);
+  s.vhl = reinterpret_cast<uint16_t*>(p); p += (size_t)2 * kTT * rk_max(max_rank) * sizeof(uint16_t);
+  s.buf = reinterpret_cast<uint16_t*>(p);
   return s;
 }
 
-__device__ __forceinline__ void load_tokens(const ApplyArgs& g, const Tile& t, int* tok) {
-  if (threadIdx.x < kTT) {
-    int tk = -1;
-    if ((int)threadIdx.x < t.L) {
-      tk = g.perm[t.p0 + threadIdx.x];
-      if (tk < 0 || tk >= g.T) tk = -1;
-    }
-    tok[threadIdx.x] = tk;
-  }
+constexpr int ilog2(int v) { return v <= 1 ? 0 : 1 + ilog2(v / 2); }
+
+// ---------------------------------------------------------------------------
+// single-token tiles: vector ALU
+// ---------------------------------------------------------------------------
+
+// Expand lane layout: row slots per column octet and this thread's octet.
+struct ExpandMap {
+  int RSB, CPW, co0, rb, njb;
+};
+
+__device__ __forceinline__ ExpandMap expand_map(const ApplyArgs& g, const Tile& t) {
+  ExpandMap m;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  m.RSB = 1 << g.rsb_log2;
+  m.CPW = 64 / m.RSB;
+  m.co0 = w * m.CPW + lane % m.CPW;
+  m.rb = lane / m.CPW;
+  m.njb = m.rb < t.r ? (t.r - m.rb + m.RSB - 1) / m.RSB : 0;
+  return m;
 }
 
-// x rows of tokens g0..g0+kTG-1 into xs[k][tt], zero for missing tokens.
-__device__ void stage_x(const ApplyArgs& g, const int* tok, int g0, int L, uint16_t* xs) {
-  const int n8 = g.h_in >> 3;
-  const int total = kTG * n8;
-  for (int c = threadIdx.x; c < total; c += kNT) {
-    const int tt = c / n8, kc = c - tt * n8;
-    const int l = g0 + tt;
-    const int tk = l < L ? tok[l] : -1;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (tk >= 0) v = ldg16(g.x + (int64_t)tk * g.ldx + kc * 8);
-    uint16_t* d = xs + (kc * 8) * kTG + tt;
-    d[0 * kTG] = (uint16_t)(v.x & 0xffffu); d[1 * kTG] = (uint16_t)(v.x >> 16);
-    d[2 * kTG] = (uint16_t)(v.y & 0xffffu); d[3 * kTG] = (uint16_t)(v.y >> 16);
-    d[4 * kTG] = (uint16_t)(v.z & 0xffffu); d[5 * kTG] = (uint16_t)(v.z >> 16);
-    d[6 * kTG] = (uint16_t)(v.w & 0xffffu); d[7 * kTG] = (uint16_t)(v.w >> 16);
-  }
+// This thread's first kBP chunks of B_i (first column batch) and its y word.
+__device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, uint4 (&bpre)[kBP]) {
+  const ExpandMap m = expand_map(g, t);
+  const bool col_ok = m.co0 < (g.h_out >> 3);
+  const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)m.co0 * 8;
+  const int64_t bstep = (int64_t)m.RSB * g.h_out;
+#pragma unroll
+  for (int j = 0; j < kBP; ++j)
+    bpre[j] = (col_ok && j < m.njb) ? ldg16(bp + j * bstep) : make_uint4(0, 0, 0, 0);
 }
 
-// One butterfly step over lane mask M on N values: the lane whose mask bit is
-// set keeps the upper half, the other the lower half, each adding the half
-// its partner sends.
+__device__ __forceinline__ uint4 prefetch_y(const ApplyArgs& g, const Tile& t, int tk) {
+  const ExpandMap m = expand_map(g, t);
+  const bool ok = m.co0 < (g.h_out >> 3) && m.rb == 0 && tk >= 0;
+  return ok ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)m.co0 * 8) : make_uint4(0, 0, 0, 0);
+}
+
+// One butterfly step over lane mask M on the first N of 8 values.
 template <int N, int M>
-__device__ __forceinline__ void halve(float (&val)[kTG * 8], int lane) {
+__device__ __forceinline__ void halve(float (&val)[8], int lane) {
   const bool up = (lane & M) != 0;
 #pragma unroll
   for (int i = 0; i < N / 2; ++i) {
@@ -436,173 +479,559 @@ __device__ __forceinline__ void halve(float (&val)[kTG * 8], int lane) {
   }
 }
 
-// v[l][c] for the whole tile into sm.vs (c < r, l < L; zero elsewhere).
+// Butterfly over the row-slot lane bits (masks R_OCT << s, s < S): halve the
+// 8 values while two or more remain, all-reduce over the remaining bits.  On
+// return the lane holds 8 >> H reduced values starting at index base, and
+// writer tells whether it is the one lane of its all-reduce group to store.
+template <int R_OCT, int S, int s>
+__device__ __forceinline__ void butterfly(float (&val)[8], int lane, int& base, bool& writer) {
+  if constexpr (s < S) {
+    constexpr int H = S < 3 ? S : 3;
+    constexpr int M = R_OCT << s;
+    if constexpr (s < H) {
+      constexpr int N = 8 >> s;
+      halve<N, M>(val, lane);
+      if (lane & M) base += N / 2;
+    } else {
+      val[0] += __shfl_xor(val[0], M, 64);
+      if (lane & M) writer = false;
+    }
+    butterfly<R_OCT, S, s + 1>(val, lane, base, writer);
+  }
+}
+
+// acc[e] += x[row] * A[row][oct*8 + e] for chunks jb..jb+kCH-1 of the window.
 template <int R_OCT>
-__device__ void shrink_tile(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+__device__ __forceinline__ void fma_a1(float (&val)[8], const uint4* a, const uint16_t* xs,
+                                       int q0, int w0, int jb, int nj) {
+#pragma unroll
+  for (int j = 0; j < kCH; ++j) {
+    if (jb + j < nj) {
+      const int row = (q0 + (int)threadIdx.x + (jb + j) * kNT) / R_OCT - w0;
+      const float xf = __uint_as_float((uint32_t)xs[row] << 16);
+      float af[8];
+      unpack8(a[j], af);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) val[e] = fmaf(xf, af[e], val[e]);
+    }
+  }
+}
+
+// v[0][c] of a single-token tile into sm.vs.  With prefetch set, this
+// thread's first kBP chunks of B_i and its y word are requested right after
+// the first chunks of A_i.
+template <int R_OCT>
+__device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                            uint4 (&bpre)[kBP], uint4& ypre, bool prefetch) {
   constexpr int R = 8 * R_OCT;
-  constexpr int RSW = 64 / R_OCT;          // row slots inside a wavefront
-  constexpr int HALV = RSW >= 32 ? 5 : (RSW == 16 ? 4 : (RSW == 8 ? 3 : 2));
-  constexpr int VL = (kTG * 8) >> HALV;    // values a lane keeps
+  constexpr int S = ilog2(64 / R_OCT);     // row-slot bits inside a wavefront
+  constexpr int H = S < 3 ? S : 3;
+  constexpr int VL = 8 >> H;               // values a lane keeps
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int oct = tid % R_OCT;
-  const int n_chunks = g.h_in * R_OCT;     // 16-byte chunks of A_i
-  const int nj = tid < n_chunks ? (n_chunks - tid + kNT - 1) / kNT : 0;
-  const uint16_t* ap = t.Ai + (int64_t)tid * 8;
+  const int tk = sm.tok[0];
+  const int XW = g.h_in < kXW ? g.h_in : kXW;
+  uint16_t* xs = sm.buf;
+  float* red = reinterpret_cast<float*>(sm.buf + kXW);
 
-  for (int g0 = 0; g0 < t.L; g0 += kTG) {
-    stage_x(g, sm.tok, g0, t.L, sm.xs);
-    __syncthreads();
-    float val[kTG * 8];
+  float val[8];
 #pragma unroll
-    for (int i = 0; i < kTG * 8; ++i) val[i] = 0.f;
-    for (int jb = 0; jb < nj; jb += kCH) {
-      uint4 a[kCH];
+  for (int i = 0; i < 8; ++i) val[i] = 0.f;
+  for (int w0 = 0; w0 < g.h_in; w0 += XW) {
+    const int w1 = min(g.h_in, w0 + XW);
+    const int q0 = w0 * R_OCT;                         // first chunk of the window
+    const int nq = (w1 - w0) * R_OCT;
+    const int nj = tid < nq ? (nq - tid + kNT - 1) / kNT : 0;
+    const int nx = (w1 - w0) >> 3;                     // x chunks of the window
+    const uint16_t* ap = t.Ai + ((int64_t)q0 + tid) * 8;
+    uint4 xr[kXW / 8 / kNT], apre[kAP];
+#pragma unroll
+    for (int i = 0; i < kXW / 8 / kNT; ++i) {
+      const int c = tid + i * kNT;
+      xr[i] = (c < nx && tk >= 0) ? ldg16(g.x + (int64_t)tk * g.ldx + w0 + c * 8)
+                                  : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kAP; ++j)
+      apre[j] = j < nj ? ldg16(ap + (int64_t)j * kNT * 8) : make_uint4(0, 0, 0, 0);
+    if (prefetch && w0 == 0) {
+      prefetch_b(g, t, bpre);
+      ypre = prefetch_y(g, t, tk);
+    }
+#pragma unroll
+    for (int i = 0; i < kXW / 8 / kNT; ++i) {
+      const int c = tid + i * kNT;
+      if (c < nx) *reinterpret_cast<uint4*>(xs + c * 8) = xr[i];
+    }
+    lds_sync();
+    fma_a1<R_OCT>(val, apre, xs, q0, w0, 0, nj);
+    fma_a1<R_OCT>(val, apre + kCH, xs, q0, w0, kCH, nj);
+    if (nj > kAP) {
+      uint4 a0[kCH], a1[kCH];
 #pragma unroll
       for (int j = 0; j < kCH; ++j)
-        a[j] = (jb + j < nj) ? ldg16(ap + (int64_t)(jb + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
+        a0[j] = (kAP + j < nj) ? ldg16(ap + (int64_t)(kAP + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
+      for (int jb = kAP; jb < nj; jb += 2 * kCH) {
 #pragma unroll
-      for (int j = 0; j < kCH; ++j) {
-        if (jb + j < nj) {
-          const int row = (tid + (jb + j) * kNT) / R_OCT;
-          const uint2 xv = *reinterpret_cast<const uint2*>(sm.xs + row * kTG);
-          const float xf[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
-          float af[8];
-          unpack8(a[j], af);
+        for (int j = 0; j < kCH; ++j)
+          a1[j] = (jb + kCH + j < nj) ? ldg16(ap + (int64_t)(jb + kCH + j) * kNT * 8)
+                                      : make_uint4(0, 0, 0, 0);
+        fma_a1<R_OCT>(val, a0, xs, q0, w0, jb, nj);
 #pragma unroll
-          for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) val[tt * 8 + e] = fmaf(xf[tt], af[e], val[tt * 8 + e]);
-        }
+        for (int j = 0; j < kCH; ++j)
+          a0[j] = (jb + 2 * kCH + j < nj) ? ldg16(ap + (int64_t)(jb + 2 * kCH + j) * kNT * 8)
+                                          : make_uint4(0, 0, 0, 0);
+        fma_a1<R_OCT>(val, a1, xs, q0, w0, jb + kCH, nj);
       }
     }
-    // reduce-scatter across the row slots of the wavefront
-    int base = 0;
-    if constexpr (HALV >= 1) { halve<32, R_OCT * 1>(val, lane); base += (lane & (R_OCT * 1)) ? 16 : 0; }
-    if constexpr (HALV >= 2) { halve<16, R_OCT * 2>(val, lane); base += (lane & (R_OCT * 2)) ? 8 : 0; }
-    if constexpr (HALV >= 3) { halve<8, R_OCT * 4>(val, lane); base += (lane & (R_OCT * 4)) ? 4 : 0; }
-    if constexpr (HALV >= 4) { halve<4, R_OCT * 8>(val, lane); base += (lane & (R_OCT * 8)) ? 2 : 0; }
-    if constexpr (HALV >= 5) { halve<2, R_OCT * 16>(val, lane); base += (lane & (R_OCT * 16)) ? 1 : 0; }
-    bool writer = true;
-    if constexpr (RSW == 64) {             // r = 8: one more all-reduce step
-      val[0] += __shfl_xor(val[0], 32, 64);
-      writer = (lane & 32) == 0;
-    }
-    __syncthreads();                        // xs is dead; red may overwrite it
-    if (writer) {
+    lds_sync();                                        // xs free
+  }
+  int base = 0;
+  bool writer = true;
+  butterfly<R_OCT, S, 0>(val, lane, base, writer);
+  if (writer) {
 #pragma unroll
-      for (int j = 0; j < VL; ++j) {
-        const int idx = base + j;
-        const int tt = idx >> 3, e = idx & 7;
-        sm.red[(w * kTG + tt) * R + oct * 8 + e] = val[j];
-      }
-    }
-    __syncthreads();
-    for (int o = tid; o < kTG * R; o += kNT) {
-      const int tt = o / R, c = o - tt * R;
-      if (g0 + tt < t.L) {
-        float s = sm.red[tt * R + c];
+    for (int j = 0; j < VL; ++j) red[w * R + oct * 8 + base + j] = val[j];
+  }
+  lds_sync();
+  for (int c = tid; c < R; c += kNT) {
+    float s = red[c];
 #pragma unroll
-        for (int ww = 1; ww < kW; ++ww) s += sm.red[(ww * kTG + tt) * R + c];
-        sm.vs[c * kTT + g0 + tt] = s;
-      }
+    for (int ww = 1; ww < kW; ++ww) s += red[ww * R + c];
+    sm.vs[c * kTT] = s;
+  }
+  lds_sync();
+}
+
+// d[e] += v[row] * B_i[row][co*8 + e] for this thread's rows jb..jb+kCH-1.
+__device__ __forceinline__ void fma_b1(float (&d)[8], const uint4* b, const Smem& sm,
+                                       const ExpandMap& m, int jb) {
+#pragma unroll
+  for (int j = 0; j < kCH; ++j) {
+    if (jb + j < m.njb) {
+      const float vf = sm.vs[(m.rb + (jb + j) * m.RSB) * kTT];
+      float bf[8];
+      unpack8(b[j], bf);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = fmaf(vf, bf[e], d[e]);
     }
-    __syncthreads();                        // red/xs free for the next group
   }
 }
 
-__device__ __forceinline__ void shrink_dispatch(const ApplyArgs& g, const Tile& t,
-                                                const Smem& sm) {
-  switch (t.r >> 3) {
-    case 1: shrink_tile<1>(g, t, sm); break;
-    case 2: shrink_tile<2>(g, t, sm); break;
-    case 4: shrink_tile<4>(g, t, sm); break;
-    case 8: shrink_tile<8>(g, t, sm); break;
-    case 16: shrink_tile<16>(g, t, sm); break;
-    default: break;  // excluded by load_tile
-  }
-}
-
-// y[tok, cols] = bf16(y + s * v B_i[:, cols]) for every token of the tile.
-__device__ void expand_tile(const ApplyArgs& g, const Tile& t, const Smem& sm) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int RSB = 1 << g.rsb_log2;
-  const int CPW = 64 / RSB;                  // column octets per wavefront
+// y[tok, cols] = bf16(y + s * v B_i[:, cols]) for a single-token tile.  The
+// first column batch uses the kBP chunks of B_i fetched before the shrink.
+__device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                            const uint4 (&bpre)[kBP], uint4 ypre, bool have_y) {
+  const ExpandMap m = expand_map(g, t);
   const int n_oct = g.h_out >> 3;
-  const int co_l = lane % CPW, rb = lane / CPW;
-  const int r = t.r;
-  const int njb = rb < r ? (r - rb + RSB - 1) / RSB : 0;
-  for (int co = w * CPW + co_l, cb = 0; cb * kW * CPW < n_oct; ++cb, co += kW * CPW) {
+  const int64_t bstep = (int64_t)m.RSB * g.h_out;
+  const int tk = sm.tok[0];
+  for (int cb = 0, co = m.co0; cb * kW * m.CPW < n_oct; ++cb, co += kW * m.CPW) {
     const bool col_ok = co < n_oct;
-    const uint16_t* bp = t.Bi + (int64_t)rb * g.h_out + (int64_t)co * 8;
-    const int64_t bstep = (int64_t)RSB * g.h_out;
-    for (int g0 = 0; g0 < t.L; g0 += kTG) {
-      float d[kTG * 8];
+    const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)co * 8;
+    float d[8];
 #pragma unroll
-      for (int i = 0; i < kTG * 8; ++i) d[i] = 0.f;
-      if (col_ok) {
-        for (int jb = 0; jb < njb; jb += kCH) {
-          uint4 b[kCH];
-#pragma unroll
-          for (int j = 0; j < kCH; ++j)
-            b[j] = (jb + j < njb) ? ldg16(bp + (int64_t)(jb + j) * bstep) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-          for (int j = 0; j < kCH; ++j) {
-            if (jb + j < njb) {
-              const int c = rb + (jb + j) * RSB;
-              const float4 vv = *reinterpret_cast<const float4*>(sm.vs + c * kTT + g0);
-              const float vf[4] = {vv.x, vv.y, vv.z, vv.w};
-              float bf[8];
-              unpack8(b[j], bf);
-#pragma unroll
-              for (int tt = 0; tt < kTG; ++tt)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) d[tt * 8 + e] = fmaf(vf[tt], bf[e], d[tt * 8 + e]);
-            }
-          }
-        }
+    for (int i = 0; i < 8; ++i) d[i] = 0.f;
+    if (col_ok) {
+      int jb0 = 0;
+      if (cb == 0) {
+        fma_b1(d, bpre, sm, m, 0);
+        fma_b1(d, bpre + kCH, sm, m, kCH);
+        jb0 = kBP;
       }
-      // all-reduce across the row slots of each column octet
-      for (int m = CPW; m < 64; m <<= 1) {
+      for (int jb = jb0; jb < m.njb; jb += kCH) {
+        uint4 b[kCH];
 #pragma unroll
-        for (int i = 0; i < kTG * 8; ++i) d[i] += __shfl_xor(d[i], m, 64);
+        for (int j = 0; j < kCH; ++j)
+          b[j] = (jb + j < m.njb) ? ldg16(bp + (int64_t)(jb + j) * bstep) : make_uint4(0, 0, 0, 0);
+        fma_b1(d, b, sm, m, jb);
       }
-      if (col_ok && rb == 0) {
+    }
+    // all-reduce across the row slots of each column octet
+    for (int msk = m.CPW; msk < 64; msk <<= 1) {
 #pragma unroll
-        for (int tt = 0; tt < kTG; ++tt) {
-          if (g0 + tt < t.L) {
-            const int tk = sm.tok[g0 + tt];
-            if (tk >= 0) {
-              uint16_t* yp = g.y + (int64_t)tk * g.ldy + (int64_t)co * 8;
-              const uint4 yv = ldg16(yp);
-              float yf[8];
-              unpack8(yv, yf);
-              uint32_t ob[8];
+      for (int i = 0; i < 8; ++i) d[i] += __shfl_xor(d[i], msk, 64);
+    }
+    if (col_ok && m.rb == 0 && tk >= 0) {
+      uint16_t* yp = g.y + (int64_t)tk * g.ldy + (int64_t)co * 8;
+      const uint4 yv = (have_y && cb == 0) ? ypre : ldg16(yp);
+      float yf[8];
+      unpack8(yv, yf);
+      uint32_t ob[8];
 #pragma unroll
-              for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[tt * 8 + e], yf[e]));
-              uint4 out;
-              out.x = ob[0] | (ob[1] << 16);
-              out.y = ob[2] | (ob[3] << 16);
-              out.z = ob[4] | (ob[5] << 16);
-              out.w = ob[6] | (ob[7] << 16);
-              *reinterpret_cast<uint4*>(yp) = out;
-            }
-          }
-        }
-      }
+      for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[e], yf[e]));
+      uint4 out;
+      out.x = ob[0] | (ob[1] << 16);
+      out.y = ob[2] | (ob[3] << 16);
+      out.z = ob[4] | (ob[5] << 16);
+      out.w = ob[6] | (ob[7] << 16);
+      *reinterpret_cast<uint4*>(yp) = out;
     }
   }
 }
 
-// Common prologue: tile, tokens, zeroed v.  Returns false if the work group
-// has nothing to do.
-__device__ __forceinline__ bool tile_prologue(const ApplyArgs& g, Tile& t, Smem& sm,
-                                              void* lds) {
-  if (!load_tile(g, t)) return false;
-  sm = carve(lds, g.max_rank);
-  load_tokens(g, t, sm.tok);
+__device__ __forceinline__ void valu_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                          bool do_shrink, bool do_expand) {
+  uint4 bpre[kBP], ypre = make_uint4(0, 0, 0, 0);
+  if (do_shrink) {
+    switch (t.r >> 3) {
+      case 1: shrink_valu<1>(g, t, sm, bpre, ypre, do_expand); break;
+      case 2: shrink_valu<2>(g, t, sm, bpre, ypre, do_expand); break;
+      case 4: shrink_valu<4>(g, t, sm, bpre, ypre, do_expand); break;
+      case 8: shrink_valu<8>(g, t, sm, bpre, ypre, do_expand); break;
+      default: shrink_valu<16>(g, t, sm, bpre, ypre, do_expand); break;
+    }
+  } else {
+    prefetch_b(g, t, bpre);
+  }
+  if (do_expand) expand_valu(g, t, sm, bpre, ypre, do_shrink);
+}
+
+// ---------------------------------------------------------------------------
+// multi-token tiles: matrix cores
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// MFMA operand holding rows rbase + 8 * (lane / 16) .. + 8 of column
+// cbase + lane % 16 of a row-major bf16 matrix in LDS (row stride S elements,
+// S and cbase multiples of 4): two transposed 64-bit reads; in each group of
+// 16 lanes, lane 4j + c reads row j, columns 4c..4c+3, and lane i receives
+// column i of the four rows.
+__device__ __forceinline__ bf16x8_t tr_operand(const uint16_t* m, int S, int rbase, int cbase) {
+  const int l = threadIdx.x & 63, grp = l >> 4, lp = l & 15;
+  const uint16_t* p = m + (rbase + 8 * grp + (lp >> 2)) * S + cbase + 4 * (lp & 3);
+  const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
+  const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 4 * S));
+  const uint2 a = __builtin_bit_cast(uint2, lo), b = __builtin_bit_cast(uint2, hi);
+  return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// Shrink of a multi-token tile: MT M tiles of 16 tokens, NTN N tiles of 16
+// columns (r = 8 uses the first half of one tile).  Writes v to sm.vs (fp32)
+// and its high/low bf16 split to sm.vhl.
+template <int MT, int NTN>
+__device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r = t.r;
+  const int S = r < 16 ? 16 : r;                   // LDS row stride of A_i chunks
+  const int RK = rk_max(g.max_rank);
+  // rows per chunk: a multiple of kRK * kW, at most kChunk / S, and at most
+  // 4 K steps of x operands per wave over all M tiles
+  const int KC = min(kChunk / S, 1024 / MT);
+  const int nchunks = (g.h_in + KC - 1) / KC;
+  uint16_t* As = sm.buf;
+
+  f32x4_t acc[MT][NTN];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NTN; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // x operands of this wave's K steps of one chunk: [step][M tile]
+  constexpr int XK = 4 / MT;
+  uint4 xcur[XK][MT], xnxt[XK][MT], areg[8];
+  const int grp = lane >> 4;
+  int toks[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int ti = mt * 16 + (lane & 15);
+    toks[mt] = ti < t.L ? sm.tok[ti] : -1;
+  }
+  auto load_x = [&](int k0, uint4 (&xo)[XK][MT]) {
+#pragma unroll
+    for (int i = 0; i < XK; ++i) {
+      const int k = k0 + (w + i * kW) * kRK + 8 * grp;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+        xo[i][mt] = (toks[mt] >= 0 && k < g.h_in && k < k0 + KC)
+                        ? ldg16(g.x + (int64_t)toks[mt] * g.ldx + k)
+                        : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto load_a = [&](int k0) {
+    const int rows = min(KC, g.h_in - k0);
+    const int n16 = rows * (r >> 3);
+    const uint16_t* src = t.Ai + (int64_t)k0 * r;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int q = tid + j * kNT;
+      areg[j] = q < n16 ? ldg16(src + (int64_t)q * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_a = [&](int k0) {
+    const int rows = min(KC, g.h_in - k0);
+    const int n16 = rows * (r >> 3);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int q = tid + j * kNT;
+      if (q < n16) {
+        if (r == 8) {
+          *reinterpret_cast<uint4*>(As + q * 16) = areg[j];
+          *reinterpret_cast<uint4*>(As + q * 16 + 8) = make_uint4(0, 0, 0, 0);
+        } else {
+          *reinterpret_cast<uint4*>(As + q * 8) = areg[j];
+        }
+      }
+    }
+    // zero the rows that pad the last K step of the chunk
+    const int padded = (rows + kRK - 1) / kRK * kRK;
+    for (int q = tid; q < (padded - rows) * (S >> 3); q += kNT)
+      *reinterpret_cast<uint4*>(As + rows * S + q * 8) = make_uint4(0, 0, 0, 0);
+  };
+
+  load_x(0, xcur);
+  load_a(0);
+  for (int c = 0; c < nchunks; ++c) {
+    const int k0 = c * KC;
+    store_a(k0);
+    lds_sync();
+    if (c + 1 < nchunks) {
+      load_x(k0 + KC, xnxt);
+      load_a(k0 + KC);
+    }
+    const int ksn = (min(KC, g.h_in - k0) + kRK - 1) / kRK;
+#pragma unroll
+    for (int i = 0; i < XK; ++i) {
+      const int ks = w + i * kW;
+      if (ks < ksn) {
+#pragma unroll
+        for (int nt = 0; nt < NTN; ++nt) {
+          const bf16x8_t b = tr_operand(As, S, ks * kRK, nt * 16);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xcur[i][mt]), b,
+                                                                  acc[mt][nt], 0, 0, 0);
+        }
+      }
+    }
+    lds_sync();
+#pragma unroll
+    for (int i = 0; i < XK; ++i)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) xcur[i][mt] = xnxt[i][mt];
+  }
+
+  // pairwise tree over the wavefronts: 4 -> 2 -> 1 slots, fixed order
+  f32x4_t* slot = reinterpret_cast<f32x4_t*>(sm.buf);
+  for (int half = kW / 2; half >= 1; half >>= 1) {
+    if (w >= half && w < 2 * half) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTN; ++nt)
+          slot[(((w - half) * MT + mt) * NTN + nt) * 64 + lane] = acc[mt][nt];
+    }
+    lds_sync();
+    if (w < half) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTN; ++nt)
+          acc[mt][nt] += slot[((w * MT + mt) * NTN + nt) * 64 + lane];
+    }
+    lds_sync();
+  }
+  if (w == 0) {
+    uint16_t* vhi = sm.vhl;
+    uint16_t* vlo = sm.vhl + kTT * RK;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NTN; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tt = mt * 16 + 4 * grp + i, c = nt * 16 + (lane & 15);
+          if (tt < t.L && c < r) {
+            const float val = acc[mt][nt][i];
+            const uint32_t hb = to_bf16(val);
+            const float hv = __uint_as_float(hb << 16);
+            sm.vs[c * kTT + tt] = val;
+            vhi[tt * RK + c] = (uint16_t)hb;
+            vlo[tt * RK + c] = (uint16_t)to_bf16(val - hv);
+          }
+        }
+  }
+  lds_sync();
+}
+
+// v (fp32, already in sm.vs) to its high/low bf16 split in sm.vhl.
+__device__ __forceinline__ void split_v(const Tile& t, const Smem& sm, int RK) {
+  for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
+    const int tt = o / t.r, c = o - tt * t.r;
+    const float val = sm.vs[c * kTT + tt];
+    const uint32_t hb = to_bf16(val);
+    sm.vhl[tt * RK + c] = (uint16_t)hb;
+    sm.vhl[kTT * RK + tt * RK + c] = (uint16_t)to_bf16(val - __uint_as_float(hb << 16));
+  }
+}
+
+// Expand of a multi-token tile with MT token tiles of 16: D^T[j][token] =
+// sum_c B_i[c][j] (vhi + vlo)[token][c], then y = bf16(y + s D).
+template <int MT>
+__device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4;
+  const int r = t.r;
+  const int RK = rk_max(g.max_rank);
+  const int rk = r < kRK ? kRK : r;                // K extent, zero rows above r
+  const int JC = min(kChunk / rk, (g.h_out + 15) / 16 * 16);   // columns per chunk
+  const int nchunks = (g.h_out + JC - 1) / JC;
+  uint16_t* Bs = sm.buf;
+  const uint16_t* vhi = sm.vhl;
+  const uint16_t* vlo = sm.vhl + kTT * RK;
+  constexpr int JT = 8;                            // j tiles per wave per chunk (max)
+  uint4 breg[8];
+  uint2 yv[JT][MT];
+  int toks[MT];
+#pragma unroll
+  for (int nt = 0; nt < MT; ++nt) {
+    const int ti = nt * 16 + (lane & 15);
+    toks[nt] = ti < t.L ? sm.tok[ti] : -1;
+  }
+  auto load_b = [&](int j0) {
+    const int cols = min(JC, g.h_out - j0);
+    const int per_row = cols >> 3;
+    const int n16 = r * per_row;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int q = tid + j * kNT;
+      if (q < n16) {
+        const int c = q / per_row, col = q - c * per_row;
+        breg[j] = ldg16(t.Bi + (int64_t)c * g.h_out + j0 + col * 8);
+      } else {
+        breg[j] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto store_b = [&](int j0) {
+    const int cols = min(JC, g.h_out - j0);
+    const int per_row = cols >> 3;
+    const int n16 = r * per_row;
+    const int S = (cols + 15) / 16 * 16;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int q = tid + j * kNT;
+      if (q < n16) {
+        const int c = q / per_row, col = q - c * per_row;
+        *reinterpret_cast<uint4*>(Bs + c * S + col * 8) = breg[j];
+      }
+    }
+    // zero padding: columns [cols, S) of rows < r, and rows [r, rk)
+    if (S != cols)
+      for (int c = tid; c < r; c += kNT)
+        *reinterpret_cast<uint4*>(Bs + c * S + cols) = make_uint4(0, 0, 0, 0);
+    for (int q = tid; q < (rk - r) * (S >> 3); q += kNT)
+      *reinterpret_cast<uint4*>(Bs + r * S + q * 8) = make_uint4(0, 0, 0, 0);
+  };
+
+  load_b(0);
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int j0 = ch * JC;
+    const int cols = min(JC, g.h_out - j0);
+    const int S = (cols + 15) / 16 * 16;
+    const int njt = S / 16;
+    store_b(j0);
+    lds_sync();
+    // y words of this wave's j tiles, then the next chunk of B_i
+#pragma unroll
+    for (int i = 0; i < JT; ++i) {
+      const int jt = w + i * kW;
+      const int j = j0 + jt * 16 + 4 * grp;
+#pragma unroll
+      for (int nt = 0; nt < MT; ++nt)
+        yv[i][nt] = (jt < njt && j < g.h_out && toks[nt] >= 0)
+                        ? *reinterpret_cast<const uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j)
+                        : make_uint2(0, 0);
+    }
+    if (ch + 1 < nchunks) load_b(j0 + JC);
+#pragma unroll
+    for (int i = 0; i < JT; ++i) {
+      const int jt = w + i * kW;
+      if (jt < njt) {
+        f32x4_t acc[MT];
+#pragma unroll
+        for (int nt = 0; nt < MT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int kc = 0; kc < rk; kc += kRK) {
+          const bf16x8_t a = tr_operand(Bs, S, kc, jt * 16);
+#pragma unroll
+          for (int nt = 0; nt < MT; ++nt) {
+            const int tt = nt * 16 + (lane & 15);
+            const uint4 h = *reinterpret_cast<const uint4*>(vhi + tt * RK + kc + 8 * grp);
+            const uint4 lo = *reinterpret_cast<const uint4*>(vlo + tt * RK + kc + 8 * grp);
+            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_bf16x8(h), acc[nt], 0, 0, 0);
+            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_bf16x8(lo), acc[nt], 0, 0, 0);
+          }
+        }
+        const int j = j0 + jt * 16 + 4 * grp;
+#pragma unroll
+        for (int nt = 0; nt < MT; ++nt) {
+          if (toks[nt] >= 0 && j < g.h_out) {
+            const uint2 yw = yv[i][nt];
+            const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
+            const uint32_t o0 = to_bf16(fmaf(t.s, acc[nt][0], y0));
+            const uint32_t o1 = to_bf16(fmaf(t.s, acc[nt][1], y1));
+            const uint32_t o2 = to_bf16(fmaf(t.s, acc[nt][2], y2));
+            const uint32_t o3 = to_bf16(fmaf(t.s, acc[nt][3], y3));
+            *reinterpret_cast<uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j) =
+                make_uint2(o0 | (o1 << 16), o2 | (o3 << 16));
+          }
+        }
+      }
+    }
+    lds_sync();
+  }
+}
+
+__device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                          bool do_shrink, bool do_expand) {
+  const int RK = rk_max(g.max_rank);
+  // v's bf16 split is read for every token row < 16 * MT and column < K extent
+  for (int o = threadIdx.x; o < 2 * kTT * RK; o += kNT) sm.vhl[o] = 0;
+  lds_sync();
+  const bool two = t.L > 16;
+  if (do_shrink) {
+    const int ntn = t.r <= 16 ? 1 : t.r / 16;
+    if (two) {
+      switch (ntn) {
+        case 1: shrink_mfma<2, 1>(g, t, sm); break;
+        case 2: shrink_mfma<2, 2>(g, t, sm); break;
+        case 4: shrink_mfma<2, 4>(g, t, sm); break;
+        default: shrink_mfma<2, 8>(g, t, sm); break;
+      }
+    } else {
+      switch (ntn) {
+        case 1: shrink_mfma<1, 1>(g, t, sm); break;
+        case 2: shrink_mfma<1, 2>(g, t, sm); break;
+        case 4: shrink_mfma<1, 4>(g, t, sm); break;
+        default: shrink_mfma<1, 8>(g, t, sm); break;
+      }
+    }
+  } else {
+    split_v(t, sm, RK);
+    lds_sync();
+  }
+  if (do_expand) {
+    if (two) expand_mfma<2>(g, t, sm);
+    else expand_mfma<1>(g, t, sm);
+  }
+}
+
+__device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
+                                              const Smem& sm, bool do_shrink,
+                                              bool do_expand) {
+  if (t.L > 1) mfma_tile(g, t, sm, do_shrink, do_expand);
+  else valu_tile(g, t, sm, do_shrink, do_expand);
+}
+
+// Common prologue: token indices to LDS, v zeroed.
+__device__ __forceinline__ Smem tile_prologue(const ApplyArgs& g, int my_tok, void* lds) {
+  Smem sm = carve(lds, g.max_rank);
+  if (threadIdx.x < kTT) sm.tok[threadIdx.x] = my_tok;
   for (int o = threadIdx.x; o < g.max_rank * kTT; o += kNT) sm.vs[o] = 0.f;
-  __syncthreads();
-  return true;
+  lds_sync();
+  return sm;
 }
 
 // ---------------------------------------------------------------------------
@@ -612,9 +1041,10 @@ __device__ __forceinline__ bool tile_prologue(const ApplyArgs& g, Tile& t, Smem&
 __global__ __launch_bounds__(kNT) void shrink_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   Tile t;
-  Smem sm;
-  if (!tile_prologue(g, t, sm, apply_lds)) return;
-  shrink_dispatch(g, t, sm);
+  int my_tok;
+  if (!load_tile(g, t, my_tok)) return;
+  const Smem sm = tile_prologue(g, my_tok, apply_lds);
+  tile_dispatch(g, t, sm, true, false);
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
     const int tk = sm.tok[l];
@@ -625,24 +1055,25 @@ __global__ __launch_bounds__(kNT) void shrink_kernel(ApplyArgs g) {
 __global__ __launch_bounds__(kNT) void expand_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   Tile t;
-  Smem sm;
-  if (!tile_prologue(g, t, sm, apply_lds)) return;
+  int my_tok;
+  if (!load_tile(g, t, my_tok)) return;
+  const Smem sm = tile_prologue(g, my_tok, apply_lds);
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
     const int tk = sm.tok[l];
-    if (tk >= 0) sm.vs[c * kTT + l] = g.v[(int64_t)tk * g.ldv + c];
+    sm.vs[c * kTT + l] = tk >= 0 ? g.v[(int64_t)tk * g.ldv + c] : 0.f;
   }
-  __syncthreads();
-  expand_tile(g, t, sm);
+  lds_sync();
+  tile_dispatch(g, t, sm, false, true);
 }
 
 __global__ __launch_bounds__(kNT) void apply_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   Tile t;
-  Smem sm;
-  if (!tile_prologue(g, t, sm, apply_lds)) return;
-  shrink_dispatch(g, t, sm);
-  expand_tile(g, t, sm);
+  int my_tok;
+  if (!load_tile(g, t, my_tok)) return;
+  const Smem sm = tile_prologue(g, my_tok, apply_lds);
+  tile_dispatch(g, t, sm, true, true);
 }
 
 __global__ void zero_kernel(uint4* p, size_t n16) {
