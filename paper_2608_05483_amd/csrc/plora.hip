@@ -322,9 +322,9 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 
 constexpr int kNT = 512;             // threads per tile work group
 constexpr int kW = kNT / 64;         // wavefronts per work group
-constexpr int kAP = 16;              // A_i chunks per thread requested up front
-constexpr int kBP = 16;              // B_i chunks per thread requested up front
-constexpr int kXW = 8192;            // x row window staged in LDS (single-token path)
+constexpr int kAP = 16;              // most A_i chunks per thread requested up front
+constexpr int kBP = 16;              // most B_i chunks per thread requested up front
+constexpr int kXW = 8192;            // x row window staged in LDS (vector path)
 constexpr int kChunk = 32768;        // bf16 elements per LDS staging chunk (64 KiB)
 constexpr int kRK = 32;              // MFMA K step
 
@@ -430,8 +430,15 @@ __device__ __forceinline__ Smem carve(void* base, int max_rank) {
 constexpr int ilog2(int v) { return v <= 1 ? 0 : 1 + ilog2(v / 2); }
 
 // ---------------------------------------------------------------------------
-// single-token tiles: vector ALU
+// tiles of up to kVT tokens: vector ALU
 // ---------------------------------------------------------------------------
+
+constexpr int kVT = 4;               // longest tile on the vector path
+
+// A_i and B_i chunks per thread requested up front for TG tokens: wider
+// token groups hold more accumulators and x words, so they prefetch less.
+template <int TG> constexpr int ap_depth() { return TG <= 2 ? kAP : kAP / 2; }
+template <int TG> constexpr int bp_depth() { return TG == 1 ? kBP : kBP / 2; }
 
 // Expand lane layout: row slots per column octet and this thread's octet.
 struct ExpandMap {
@@ -449,26 +456,37 @@ __device__ __forceinline__ ExpandMap expand_map(const ApplyArgs& g, const Tile& 
   return m;
 }
 
-// This thread's first kBP chunks of B_i (first column batch) and its y word.
-__device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, uint4 (&bpre)[kBP]) {
+// This thread's first BP chunks of B_i (first column batch).
+template <int BP>
+__device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, uint4 (&bpre)[BP]) {
   const ExpandMap m = expand_map(g, t);
   const bool col_ok = m.co0 < (g.h_out >> 3);
   const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)m.co0 * 8;
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
 #pragma unroll
-  for (int j = 0; j < kBP; ++j)
+  for (int j = 0; j < BP; ++j)
     bpre[j] = (col_ok && j < m.njb) ? ldg16(bp + j * bstep) : make_uint4(0, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint4 prefetch_y(const ApplyArgs& g, const Tile& t, int tk) {
+// This thread's y words (first column octet, row slot 0) of the tile's tokens.
+template <int TG>
+__device__ __forceinline__ void prefetch_y(const ApplyArgs& g, const Tile& t, const int* tok,
+                                           uint4 (&ypre)[TG]) {
   const ExpandMap m = expand_map(g, t);
-  const bool ok = m.co0 < (g.h_out >> 3) && m.rb == 0 && tk >= 0;
-  return ok ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)m.co0 * 8) : make_uint4(0, 0, 0, 0);
+  const bool ok = m.co0 < (g.h_out >> 3) && m.rb == 0;
+#pragma unroll
+  for (int tt = 0; tt < TG; ++tt) {
+    const int tk = (ok && tt < t.L) ? tok[tt] : -1;
+    ypre[tt] = tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)m.co0 * 8)
+                       : make_uint4(0, 0, 0, 0);
+  }
 }
 
-// One butterfly step over lane mask M on the first N of 8 values.
-template <int N, int M>
-__device__ __forceinline__ void halve(float (&val)[8], int lane) {
+// One butterfly step over lane mask M on the first N of V values: the lane
+// whose mask bit is set keeps the upper half, the other the lower half, each
+// adding the half its partner sends.
+template <int V, int N, int M>
+__device__ __forceinline__ void halve(float (&val)[V], int lane) {
   const bool up = (lane & M) != 0;
 #pragma unroll
   for (int i = 0; i < N / 2; ++i) {
@@ -480,211 +498,295 @@ __device__ __forceinline__ void halve(float (&val)[8], int lane) {
 }
 
 // Butterfly over the row-slot lane bits (masks R_OCT << s, s < S): halve the
-// 8 values while two or more remain, all-reduce over the remaining bits.  On
-// return the lane holds 8 >> H reduced values starting at index base, and
+// V values while two or more remain, all-reduce over the remaining bits.  On
+// return the lane holds V >> H reduced values starting at index base, and
 // writer tells whether it is the one lane of its all-reduce group to store.
-template <int R_OCT, int S, int s>
-__device__ __forceinline__ void butterfly(float (&val)[8], int lane, int& base, bool& writer) {
+template <int V, int R_OCT, int S, int s>
+__device__ __forceinline__ void butterfly(float (&val)[V], int lane, int& base, bool& writer) {
   if constexpr (s < S) {
-    constexpr int H = S < 3 ? S : 3;
+    constexpr int H = S < ilog2(V) ? S : ilog2(V);
     constexpr int M = R_OCT << s;
     if constexpr (s < H) {
-      constexpr int N = 8 >> s;
-      halve<N, M>(val, lane);
+      constexpr int N = V >> s;
+      halve<V, N, M>(val, lane);
       if (lane & M) base += N / 2;
     } else {
-      val[0] += __shfl_xor(val[0], M, 64);
+      constexpr int VL = V >> H;
+#pragma unroll
+      for (int j = 0; j < VL; ++j) val[j] += __shfl_xor(val[j], M, 64);
       if (lane & M) writer = false;
     }
-    butterfly<R_OCT, S, s + 1>(val, lane, base, writer);
+    butterfly<V, R_OCT, S, s + 1>(val, lane, base, writer);
   }
 }
 
-// acc[e] += x[row] * A[row][oct*8 + e] for chunks jb..jb+kCH-1 of the window.
-template <int R_OCT>
-__device__ __forceinline__ void fma_a1(float (&val)[8], const uint4* a, const uint16_t* xs,
-                                       int q0, int w0, int jb, int nj) {
+// The TG bf16 x values of one row of xs (xs[k][TG]), as fp32.
+template <int TG>
+__device__ __forceinline__ void x_row(const uint16_t* xs, int row, float (&xf)[TG]) {
+  if constexpr (TG == 1) {
+    xf[0] = __uint_as_float((uint32_t)xs[row] << 16);
+  } else if constexpr (TG == 2) {
+    const uint32_t v = *reinterpret_cast<const uint32_t*>(xs + row * 2);
+    xf[0] = bf_lo(v); xf[1] = bf_hi(v);
+  } else {
+    const uint2 v = *reinterpret_cast<const uint2*>(xs + row * 4);
+    xf[0] = bf_lo(v.x); xf[1] = bf_hi(v.x); xf[2] = bf_lo(v.y); xf[3] = bf_hi(v.y);
+  }
+}
+
+// acc[tt][e] += x[tt][row] * A[row][oct*8 + e] for chunks jb..jb+kCH-1 of the
+// window starting at chunk q0 (rows relative to w0).
+template <int R_OCT, int TG>
+__device__ __forceinline__ void fma_a(float (&val)[TG * 8], const uint4* a, const uint16_t* xs,
+                                      int q0, int w0, int jb, int nj) {
 #pragma unroll
   for (int j = 0; j < kCH; ++j) {
     if (jb + j < nj) {
       const int row = (q0 + (int)threadIdx.x + (jb + j) * kNT) / R_OCT - w0;
-      const float xf = __uint_as_float((uint32_t)xs[row] << 16);
+      float xf[TG];
+      x_row<TG>(xs, row, xf);
       float af[8];
       unpack8(a[j], af);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) val[e] = fmaf(xf, af[e], val[e]);
+      for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) val[tt * 8 + e] = fmaf(xf[tt], af[e], val[tt * 8 + e]);
     }
   }
 }
 
-// v[0][c] of a single-token tile into sm.vs.  With prefetch set, this
-// thread's first kBP chunks of B_i and its y word are requested right after
-// the first chunks of A_i.
-template <int R_OCT>
+// v of a tile of L <= TG tokens into sm.vs.  Loads are requested in the
+// order they are consumed: x of the window, the first AP chunks of A_i and,
+// with prefetch set, this thread's first BP chunks of B_i and its y words.
+template <int R_OCT, int TG>
 __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                            uint4 (&bpre)[kBP], uint4& ypre, bool prefetch) {
+                                            uint4 (&bpre)[bp_depth<TG>()],
+                                            uint4 (&ypre)[TG], bool prefetch) {
   constexpr int R = 8 * R_OCT;
+  constexpr int V = TG * 8;
   constexpr int S = ilog2(64 / R_OCT);     // row-slot bits inside a wavefront
-  constexpr int H = S < 3 ? S : 3;
-  constexpr int VL = 8 >> H;               // values a lane keeps
+  constexpr int H = S < ilog2(V) ? S : ilog2(V);
+  constexpr int VL = V >> H;               // values a lane keeps
+  constexpr int XR = kXW * TG / 8 / kNT;   // x chunks per thread of a full window
+  constexpr int AP = ap_depth<TG>();
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int oct = tid % R_OCT;
-  const int tk = sm.tok[0];
   const int XW = g.h_in < kXW ? g.h_in : kXW;
-  uint16_t* xs = sm.buf;
-  float* red = reinterpret_cast<float*>(sm.buf + kXW);
+  uint16_t* xs = sm.buf;                   // [XW][TG]
+  float* red = reinterpret_cast<float*>(sm.buf);  // [kW][TG][R], after xs is dead
 
-  float val[8];
+  float val[V];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) val[i] = 0.f;
+  for (int i = 0; i < V; ++i) val[i] = 0.f;
   for (int w0 = 0; w0 < g.h_in; w0 += XW) {
     const int w1 = min(g.h_in, w0 + XW);
     const int q0 = w0 * R_OCT;                         // first chunk of the window
     const int nq = (w1 - w0) * R_OCT;
     const int nj = tid < nq ? (nq - tid + kNT - 1) / kNT : 0;
-    const int nx = (w1 - w0) >> 3;                     // x chunks of the window
+    const int n8 = (w1 - w0) >> 3;                     // x chunks per token
     const uint16_t* ap = t.Ai + ((int64_t)q0 + tid) * 8;
-    uint4 xr[kXW / 8 / kNT], apre[kAP];
+    uint4 xr[XR], apre[AP];
 #pragma unroll
-    for (int i = 0; i < kXW / 8 / kNT; ++i) {
+    for (int i = 0; i < XR; ++i) {
       const int c = tid + i * kNT;
-      xr[i] = (c < nx && tk >= 0) ? ldg16(g.x + (int64_t)tk * g.ldx + w0 + c * 8)
-                                  : make_uint4(0, 0, 0, 0);
+      const int tt = c / n8, kc = c - tt * n8;
+      const int tk = (tt < t.L && c < TG * n8) ? sm.tok[tt] : -1;
+      xr[i] = tk >= 0 ? ldg16(g.x + (int64_t)tk * g.ldx + w0 + kc * 8) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < kAP; ++j)
+    for (int j = 0; j < AP; ++j)
       apre[j] = j < nj ? ldg16(ap + (int64_t)j * kNT * 8) : make_uint4(0, 0, 0, 0);
     if (prefetch && w0 == 0) {
-      prefetch_b(g, t, bpre);
-      ypre = prefetch_y(g, t, tk);
+      prefetch_b<bp_depth<TG>()>(g, t, bpre);
+      prefetch_y<TG>(g, t, sm.tok, ypre);
     }
 #pragma unroll
-    for (int i = 0; i < kXW / 8 / kNT; ++i) {
+    for (int i = 0; i < XR; ++i) {
       const int c = tid + i * kNT;
-      if (c < nx) *reinterpret_cast<uint4*>(xs + c * 8) = xr[i];
+      if (c < TG * n8) {
+        const int tt = c / n8, kc = c - tt * n8;
+        const uint4 v = xr[i];
+        uint16_t* d = xs + (kc * 8) * TG + tt;
+        d[0 * TG] = (uint16_t)(v.x & 0xffffu); d[1 * TG] = (uint16_t)(v.x >> 16);
+        d[2 * TG] = (uint16_t)(v.y & 0xffffu); d[3 * TG] = (uint16_t)(v.y >> 16);
+        d[4 * TG] = (uint16_t)(v.z & 0xffffu); d[5 * TG] = (uint16_t)(v.z >> 16);
+        d[6 * TG] = (uint16_t)(v.w & 0xffffu); d[7 * TG] = (uint16_t)(v.w >> 16);
+      }
     }
     lds_sync();
-    fma_a1<R_OCT>(val, apre, xs, q0, w0, 0, nj);
-    fma_a1<R_OCT>(val, apre + kCH, xs, q0, w0, kCH, nj);
-    if (nj > kAP) {
+#pragma unroll
+    for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
+    if (nj > AP) {
       uint4 a0[kCH], a1[kCH];
 #pragma unroll
       for (int j = 0; j < kCH; ++j)
-        a0[j] = (kAP + j < nj) ? ldg16(ap + (int64_t)(kAP + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
-      for (int jb = kAP; jb < nj; jb += 2 * kCH) {
+        a0[j] = (AP + j < nj) ? ldg16(ap + (int64_t)(AP + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
+      for (int jb = AP; jb < nj; jb += 2 * kCH) {
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
           a1[j] = (jb + kCH + j < nj) ? ldg16(ap + (int64_t)(jb + kCH + j) * kNT * 8)
                                       : make_uint4(0, 0, 0, 0);
-        fma_a1<R_OCT>(val, a0, xs, q0, w0, jb, nj);
+        fma_a<R_OCT, TG>(val, a0, xs, q0, w0, jb, nj);
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
           a0[j] = (jb + 2 * kCH + j < nj) ? ldg16(ap + (int64_t)(jb + 2 * kCH + j) * kNT * 8)
                                           : make_uint4(0, 0, 0, 0);
-        fma_a1<R_OCT>(val, a1, xs, q0, w0, jb + kCH, nj);
+        fma_a<R_OCT, TG>(val, a1, xs, q0, w0, jb + kCH, nj);
       }
     }
     lds_sync();                                        // xs free
   }
   int base = 0;
   bool writer = true;
-  butterfly<R_OCT, S, 0>(val, lane, base, writer);
+  butterfly<V, R_OCT, S, 0>(val, lane, base, writer);
   if (writer) {
 #pragma unroll
-    for (int j = 0; j < VL; ++j) red[w * R + oct * 8 + base + j] = val[j];
+    for (int j = 0; j < VL; ++j) {
+      const int idx = base + j;
+      const int tt = idx >> 3, e = idx & 7;
+      red[(w * TG + tt) * R + oct * 8 + e] = val[j];
+    }
   }
   lds_sync();
-  for (int c = tid; c < R; c += kNT) {
-    float s = red[c];
+  for (int o = tid; o < TG * R; o += kNT) {
+    const int tt = o / R, c = o - tt * R;
+    if (tt < t.L) {
+      float s = red[tt * R + c];
 #pragma unroll
-    for (int ww = 1; ww < kW; ++ww) s += red[ww * R + c];
-    sm.vs[c * kTT] = s;
+      for (int ww = 1; ww < kW; ++ww) s += red[(ww * TG + tt) * R + c];
+      sm.vs[c * kTT + tt] = s;
+    }
   }
   lds_sync();
 }
 
-// d[e] += v[row] * B_i[row][co*8 + e] for this thread's rows jb..jb+kCH-1.
-__device__ __forceinline__ void fma_b1(float (&d)[8], const uint4* b, const Smem& sm,
-                                       const ExpandMap& m, int jb) {
+// The TG values v[c][0 .. TG) of one row of vs.
+template <int TG>
+__device__ __forceinline__ void v_row(const float* vs, int c, float (&vf)[TG]) {
+  const float* p = vs + c * kTT;
+  if constexpr (TG == 1) {
+    vf[0] = p[0];
+  } else if constexpr (TG == 2) {
+    const float2 a = *reinterpret_cast<const float2*>(p);
+    vf[0] = a.x; vf[1] = a.y;
+  } else {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    vf[0] = a.x; vf[1] = a.y; vf[2] = a.z; vf[3] = a.w;
+  }
+}
+
+// d[tt][e] += v[tt][row] * B_i[row][co*8 + e] for this thread's rows
+// jb..jb+kCH-1.
+template <int TG>
+__device__ __forceinline__ void fma_b(float (&d)[TG * 8], const uint4* b, const Smem& sm,
+                                      const ExpandMap& m, int jb) {
 #pragma unroll
   for (int j = 0; j < kCH; ++j) {
     if (jb + j < m.njb) {
-      const float vf = sm.vs[(m.rb + (jb + j) * m.RSB) * kTT];
+      float vf[TG];
+      v_row<TG>(sm.vs, m.rb + (jb + j) * m.RSB, vf);
       float bf[8];
       unpack8(b[j], bf);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) d[e] = fmaf(vf, bf[e], d[e]);
+      for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d[tt * 8 + e] = fmaf(vf[tt], bf[e], d[tt * 8 + e]);
     }
   }
 }
 
-// y[tok, cols] = bf16(y + s * v B_i[:, cols]) for a single-token tile.  The
-// first column batch uses the kBP chunks of B_i fetched before the shrink.
+// y[tok, cols] = bf16(y + s * v B_i[:, cols]) for a tile of L <= TG tokens.
+// The first column batch uses the chunks of B_i and the y words fetched
+// before the shrink.
+template <int TG>
 __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                            const uint4 (&bpre)[kBP], uint4 ypre, bool have_y) {
+                                            const uint4 (&bpre)[bp_depth<TG>()],
+                                            const uint4 (&ypre)[TG], bool have_y) {
+  constexpr int BP = bp_depth<TG>();
   const ExpandMap m = expand_map(g, t);
   const int n_oct = g.h_out >> 3;
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
-  const int tk = sm.tok[0];
   for (int cb = 0, co = m.co0; cb * kW * m.CPW < n_oct; ++cb, co += kW * m.CPW) {
     const bool col_ok = co < n_oct;
     const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)co * 8;
-    float d[8];
+    float d[TG * 8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) d[i] = 0.f;
+    for (int i = 0; i < TG * 8; ++i) d[i] = 0.f;
     if (col_ok) {
       int jb0 = 0;
       if (cb == 0) {
-        fma_b1(d, bpre, sm, m, 0);
-        fma_b1(d, bpre + kCH, sm, m, kCH);
-        jb0 = kBP;
+#pragma unroll
+        for (int jb = 0; jb < BP; jb += kCH) fma_b<TG>(d, bpre + jb, sm, m, jb);
+        jb0 = BP;
       }
       for (int jb = jb0; jb < m.njb; jb += kCH) {
         uint4 b[kCH];
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
           b[j] = (jb + j < m.njb) ? ldg16(bp + (int64_t)(jb + j) * bstep) : make_uint4(0, 0, 0, 0);
-        fma_b1(d, b, sm, m, jb);
+        fma_b<TG>(d, b, sm, m, jb);
       }
     }
     // all-reduce across the row slots of each column octet
     for (int msk = m.CPW; msk < 64; msk <<= 1) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) d[i] += __shfl_xor(d[i], msk, 64);
+      for (int i = 0; i < TG * 8; ++i) d[i] += __shfl_xor(d[i], msk, 64);
     }
-    if (col_ok && m.rb == 0 && tk >= 0) {
-      uint16_t* yp = g.y + (int64_t)tk * g.ldy + (int64_t)co * 8;
-      const uint4 yv = (have_y && cb == 0) ? ypre : ldg16(yp);
-      float yf[8];
-      unpack8(yv, yf);
-      uint32_t ob[8];
+    if (col_ok && m.rb == 0) {
+      uint4 yv[TG];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[e], yf[e]));
-      uint4 out;
-      out.x = ob[0] | (ob[1] << 16);
-      out.y = ob[2] | (ob[3] << 16);
-      out.z = ob[4] | (ob[5] << 16);
-      out.w = ob[6] | (ob[7] << 16);
-      *reinterpret_cast<uint4*>(yp) = out;
+      for (int tt = 0; tt < TG; ++tt) {
+        const int tk = tt < t.L ? sm.tok[tt] : -1;
+        yv[tt] = (have_y && cb == 0) ? ypre[tt]
+                 : (tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)co * 8)
+                            : make_uint4(0, 0, 0, 0));
+      }
+#pragma unroll
+      for (int tt = 0; tt < TG; ++tt) {
+        const int tk = tt < t.L ? sm.tok[tt] : -1;
+        if (tk >= 0) {
+          float yf[8];
+          unpack8(yv[tt], yf);
+          uint32_t ob[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[tt * 8 + e], yf[e]));
+          uint4 out;
+          out.x = ob[0] | (ob[1] << 16);
+          out.y = ob[2] | (ob[3] << 16);
+          out.z = ob[4] | (ob[5] << 16);
+          out.w = ob[6] | (ob[7] << 16);
+          *reinterpret_cast<uint4*>(g.y + (int64_t)tk * g.ldy + (int64_t)co * 8) = out;
+        }
+      }
     }
   }
 }
 
-__device__ __forceinline__ void valu_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                          bool do_shrink, bool do_expand) {
-  uint4 bpre[kBP], ypre = make_uint4(0, 0, 0, 0);
+template <int TG>
+__device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                             bool do_shrink, bool do_expand) {
+  uint4 bpre[bp_depth<TG>()], ypre[TG];
+#pragma unroll
+  for (int i = 0; i < TG; ++i) ypre[i] = make_uint4(0, 0, 0, 0);
   if (do_shrink) {
     switch (t.r >> 3) {
-      case 1: shrink_valu<1>(g, t, sm, bpre, ypre, do_expand); break;
-      case 2: shrink_valu<2>(g, t, sm, bpre, ypre, do_expand); break;
-      case 4: shrink_valu<4>(g, t, sm, bpre, ypre, do_expand); break;
-      case 8: shrink_valu<8>(g, t, sm, bpre, ypre, do_expand); break;
-      default: shrink_valu<16>(g, t, sm, bpre, ypre, do_expand); break;
+      case 1: shrink_valu<1, TG>(g, t, sm, bpre, ypre, do_expand); break;
+      case 2: shrink_valu<2, TG>(g, t, sm, bpre, ypre, do_expand); break;
+      case 4: shrink_valu<4, TG>(g, t, sm, bpre, ypre, do_expand); break;
+      case 8: shrink_valu<8, TG>(g, t, sm, bpre, ypre, do_expand); break;
+      default: shrink_valu<16, TG>(g, t, sm, bpre, ypre, do_expand); break;
     }
   } else {
-    prefetch_b(g, t, bpre);
+    prefetch_b<bp_depth<TG>()>(g, t, bpre);
   }
-  if (do_expand) expand_valu(g, t, sm, bpre, ypre, do_shrink);
+  if (do_expand) expand_valu<TG>(g, t, sm, bpre, ypre, do_shrink);
+}
+
+__device__ __forceinline__ void valu_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                          bool do_shrink, bool do_expand) {
+  if (t.L == 1) valu_tile_tg<1>(g, t, sm, do_shrink, do_expand);
+  else if (t.L == 2) valu_tile_tg<2>(g, t, sm, do_shrink, do_expand);
+  else valu_tile_tg<4>(g, t, sm, do_shrink, do_expand);
 }
 
 // ---------------------------------------------------------------------------
@@ -1021,7 +1123,7 @@ __device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, con
 __device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
                                               const Smem& sm, bool do_shrink,
                                               bool do_expand) {
-  if (t.L > 1) mfma_tile(g, t, sm, do_shrink, do_expand);
+  if (t.L > kVT) mfma_tile(g, t, sm, do_shrink, do_expand);
   else valu_tile(g, t, sm, do_shrink, do_expand);
 }
 
