@@ -5,10 +5,11 @@
 //   plora_segment  one 1024-thread work group: LSD radix sort of packed
 //                  (adapter id, token index) words in LDS, ballot-based stable
 //                  ranking per wavefront, then segment and tile lists.
-//   plora_shrink   one work group per tile (PLORA_TILE_TOKENS tokens of one
-//   plora_expand   adapter, section VI-B's per-adapter batch B_i split into
-//   plora_apply    tiles), streaming that adapter's A_i and B_i once with
-//                  128-bit loads; details above the apply kernels below.
+//   plora_shrink   persistent work groups (two per compute unit) striding
+//   plora_expand   over work items: one tile (PLORA_TILE_TOKENS tokens of one
+//   plora_apply    adapter, section VI-B's per-adapter batch B_i split into
+//                  tiles) and one slice of the y columns; details above the
+//                  apply kernels below.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -285,26 +286,38 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// apply kernels: one work group per tile
+// apply kernels
 // ---------------------------------------------------------------------------
 //
-// A work group of kNT threads owns one tile (<= PLORA_TILE_TOKENS tokens of
-// one adapter) and reads every byte of that adapter's A_i and B_i once; there
-// is no communication between work groups.  Two code paths, chosen per tile:
+// Work items.  An item is one tile and one slice of the y columns.  The
+// fused apply computes the tile's v = x A_i over all of h_in in each of its
+// items and expands it with that slice of B_i, so a tile's slices need no
+// communication.  A_i is then read by every slice of its tile: the items of
+// one tile are numbered so that they fall on work groups of one XCD (work
+// group b runs on XCD b mod 8), where the first read brings A_i into the
+// XCD's L2 and the others hit it.  The number of slices JS is chosen on the
+// device from the tile count the segmentation wrote, so that a decode batch
+// of a few dozen tiles still spreads over every compute unit, and each work
+// group takes one item; the grid is an upper bound on the item count that the
+// host derives from the tile capacity, and surplus work groups return at
+// once.
 //
-// Single-token tiles (vector ALU).  A_i, a contiguous block of h_in x r bf16
-// values, is streamed as 16-byte chunks: thread tid loads chunks tid, tid +
-// kNT, ... so it always sees the column octet tid % (r/8) and a set of rows,
-// and accumulates x[row] * A_i[row][octet] in registers.  Threads sharing an
-// octet are combined inside the wavefront by a butterfly (halving while more
-// than one value remains, then all-reducing the remaining row-slot bits) and
-// across wavefronts through LDS in wave order.  The expand gives each thread
-// one column octet of B_i and all (or a row-slot share of) its r rows.  The
-// first chunks of A_i and B_i, x and the y words are all requested before any
-// of them is needed, in the order they are consumed (the vector-memory
-// counter retires in order).
+// Two code paths, chosen per tile:
 //
-// Multi-token tiles (matrix cores, v_mfma_f32_16x16x32_bf16).  The shrink
+// Tiles of up to kVT tokens (vector ALU).  A_i, a contiguous block of h_in
+// x r bf16 values, is streamed as 16-byte chunks: thread tid loads chunks
+// tid, tid + kNT, ... so it always sees the column octet tid % (r/8) and a
+// set of rows, and accumulates x[row] * A_i[row][octet] in registers for
+// every token of the tile.  Threads sharing an octet are combined inside the
+// wavefront by a butterfly (halving while more than one value remains, then
+// all-reducing the remaining row-slot bits) and across wavefronts through
+// LDS in wave order.  The expand gives each thread one column octet of the
+// slice and all (or a row-slot share of) B_i's r rows.  The first chunks of
+// A_i and B_i, x and the y words are all requested before any of them is
+// needed, in the order they are consumed (the vector-memory counter retires
+// in order).
+//
+// Longer tiles (matrix cores, v_mfma_f32_16x16x32_bf16).  The shrink
 // computes D[token][c] = sum_k x[token][k] A_i[k][c]: x rows feed the A
 // operand straight from global memory; A_i is staged in LDS in row chunks and
 // read back transposed (ds_read_b64_tr_b16) into the B operand.  Wavefronts
@@ -316,17 +329,20 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // below fp32 accuracy.  Each lane then owns four consecutive y columns of one
 // token.
 //
-// Every reduction has a fixed order, so results are bitwise reproducible,
-// and the split calls (plora_shrink then plora_expand) run the very same
-// code on the very same values as the fused call.
+// Every reduction has a fixed order that depends only on the tile and the
+// slice width, so results are bitwise reproducible, and the split calls
+// (plora_shrink then plora_expand, which choose the same slices) run the very
+// same code on the very same values as the fused call.
 
-constexpr int kNT = 512;             // threads per tile work group
+constexpr int kNT = 256;             // threads per work group
 constexpr int kW = kNT / 64;         // wavefronts per work group
+constexpr int kWGPerCU = 2;          // resident work groups per compute unit
 constexpr int kAP = 16;              // most A_i chunks per thread requested up front
 constexpr int kBP = 16;              // most B_i chunks per thread requested up front
-constexpr int kXW = 8192;            // x row window staged in LDS (vector path)
-constexpr int kChunk = 32768;        // bf16 elements per LDS staging chunk (64 KiB)
+constexpr int kXW = 4096;            // x row window staged in LDS (vector path)
+constexpr int kChunk = 16384;        // bf16 elements per LDS staging chunk (32 KiB)
 constexpr int kRK = 32;              // MFMA K step
+constexpr int kMinSlice = 512;       // fewest y columns per work item (but h_out)
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -349,25 +365,51 @@ struct ApplyArgs {
   const float* scales;
   const int32_t* perm;
   const int4* tiles;
+  const int32_t* meta;
   int32_t T, N, h_in, h_out, max_rank, tile_cap;
-  int32_t rsb_log2;    // single-token expand: row slots per column octet (log2)
+  int32_t js_max;      // most y column slices per tile
+  int32_t slots;       // resident work groups the device holds (item target)
 };
 
 struct Tile {
   int a, p0, L;
   int r;
+  int k0, k1;          // rows of A_i (and columns of x) the shrink covers
+  int j0, j1;          // y columns the expand covers
   const uint16_t* Ai;
   const uint16_t* Bi;
   float s;
 };
 
-// Read and validate the work group's tile.  Returns false (for the whole
-// work group) for padding entries and for adapters the kernels must skip.
-// Threads below L also fetch their tile row's token index (-1 if unusable);
-// it is issued together with the adapter metadata so both arrive in one trip.
-__device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t, int& my_tok) {
-  const int u = blockIdx.x;
-  if (u >= g.tile_cap) return false;
+// The items of one launch: n_tiles tiles (as written by plora_segment),
+// rounded up to a multiple of 8, times JS column slices of W columns (a
+// multiple of 16, the last one shorter).  JS is the slot count over the
+// rounded tile count, to nearest, within [1, js_max]; so the item count is at
+// most max(4/3 slots, rounded tile count) and at most js_max times the
+// rounded tile count, whichever is less (the host sizes the grid by that).
+struct Plan {
+  int n_tiles, JS, W, n_items;
+};
+
+__device__ __forceinline__ Plan make_plan(const ApplyArgs& g, bool slices) {
+  Plan p;
+  const int nt = g.meta[4];
+  p.n_tiles = nt < 0 ? 0 : (nt > g.tile_cap ? g.tile_cap : nt);
+  const int n8 = (p.n_tiles + 7) & ~7;
+  int js = 1;
+  if (slices && n8 > 0) js = max(1, min(g.js_max, (g.slots + n8 / 2) / n8));
+  p.W = ((g.h_out + js - 1) / js + 15) & ~15;
+  p.JS = (g.h_out + p.W - 1) / p.W;
+  p.n_items = n8 * p.JS;
+  return p;
+}
+
+// Read and validate tile u.  Returns false (for the whole work group) for
+// padding entries and for adapters the kernels must skip.  Threads below L
+// also fetch their tile row's token index (-1 if unusable); it is issued
+// together with the adapter metadata so both arrive in one trip.
+__device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, int& my_tok) {
+  if (u < 0 || u >= g.tile_cap) return false;
   const int4 ti = g.tiles[u];
   t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
   if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
@@ -383,6 +425,24 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, Tile& t, int& my_t
   if (bo < 0 || (bo & 7) || bo + (int64_t)g.h_out * t.r > g.b_len) return false;
   t.Ai = g.A + ao;
   t.Bi = g.B + bo;
+  t.k0 = 0;
+  t.k1 = g.h_in;
+  return true;
+}
+
+// Item i of plan p: items are numbered in groups of eight tiles, slice-major
+// inside a group, so that item i belongs to tile 8 * (i / (8 JS)) + i % 8;
+// with a grid that is a multiple of 8, all slices of a tile then run on work
+// groups with the same blockIdx.x mod 8, that is, on one XCD.
+__device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, int i, Tile& t,
+                                          int& my_tok) {
+  const int per = 8 * p.JS;
+  const int q = i / per, rem = i - q * per;
+  const int u = 8 * q + (rem & 7);
+  if (u >= p.n_tiles) return false;
+  if (!load_tile(g, u, t, my_tok)) return false;
+  t.j0 = (rem >> 3) * p.W;
+  t.j1 = min(g.h_out, t.j0 + p.W);
   return true;
 }
 
@@ -440,15 +500,21 @@ constexpr int kVT = 4;               // longest tile on the vector path
 template <int TG> constexpr int ap_depth() { return TG <= 2 ? kAP : kAP / 2; }
 template <int TG> constexpr int bp_depth() { return TG == 1 ? kBP : kBP / 2; }
 
-// Expand lane layout: row slots per column octet and this thread's octet.
+// Expand lane layout over the slice's n_oct column octets: RSB row slots per
+// octet (the largest power of two, at most 64, that still covers every octet
+// in one pass when the slice is narrow enough), this thread's first octet
+// co0 (relative to the slice) and row slot rb.
 struct ExpandMap {
-  int RSB, CPW, co0, rb, njb;
+  int RSB, CPW, co0, rb, njb, n_oct;
 };
 
-__device__ __forceinline__ ExpandMap expand_map(const ApplyArgs& g, const Tile& t) {
+__device__ __forceinline__ ExpandMap expand_map(const Tile& t) {
   ExpandMap m;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  m.RSB = 1 << g.rsb_log2;
+  m.n_oct = (t.j1 - t.j0) >> 3;
+  int l = 0;
+  while (l < 6 && (m.n_oct << (l + 1)) <= kNT) ++l;
+  m.RSB = 1 << l;
   m.CPW = 64 / m.RSB;
   m.co0 = w * m.CPW + lane % m.CPW;
   m.rb = lane / m.CPW;
@@ -459,9 +525,9 @@ __device__ __forceinline__ ExpandMap expand_map(const ApplyArgs& g, const Tile& 
 // This thread's first BP chunks of B_i (first column batch).
 template <int BP>
 __device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, uint4 (&bpre)[BP]) {
-  const ExpandMap m = expand_map(g, t);
-  const bool col_ok = m.co0 < (g.h_out >> 3);
-  const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)m.co0 * 8;
+  const ExpandMap m = expand_map(t);
+  const bool col_ok = m.co0 < m.n_oct;
+  const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + t.j0 + (int64_t)m.co0 * 8;
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
 #pragma unroll
   for (int j = 0; j < BP; ++j)
@@ -472,12 +538,12 @@ __device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, ui
 template <int TG>
 __device__ __forceinline__ void prefetch_y(const ApplyArgs& g, const Tile& t, const int* tok,
                                            uint4 (&ypre)[TG]) {
-  const ExpandMap m = expand_map(g, t);
-  const bool ok = m.co0 < (g.h_out >> 3) && m.rb == 0;
+  const ExpandMap m = expand_map(t);
+  const bool ok = m.co0 < m.n_oct && m.rb == 0;
 #pragma unroll
   for (int tt = 0; tt < TG; ++tt) {
     const int tk = (ok && tt < t.L) ? tok[tt] : -1;
-    ypre[tt] = tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)m.co0 * 8)
+    ypre[tt] = tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + t.j0 + (int64_t)m.co0 * 8)
                        : make_uint4(0, 0, 0, 0);
   }
 }
@@ -571,15 +637,15 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
   constexpr int AP = ap_depth<TG>();
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int oct = tid % R_OCT;
-  const int XW = g.h_in < kXW ? g.h_in : kXW;
+  const int XW = t.k1 - t.k0 < kXW ? t.k1 - t.k0 : kXW;
   uint16_t* xs = sm.buf;                   // [XW][TG]
   float* red = reinterpret_cast<float*>(sm.buf);  // [kW][TG][R], after xs is dead
 
   float val[V];
 #pragma unroll
   for (int i = 0; i < V; ++i) val[i] = 0.f;
-  for (int w0 = 0; w0 < g.h_in; w0 += XW) {
-    const int w1 = min(g.h_in, w0 + XW);
+  for (int w0 = t.k0; w0 < t.k1; w0 += XW) {
+    const int w1 = min(t.k1, w0 + XW);
     const int q0 = w0 * R_OCT;                         // first chunk of the window
     const int nq = (w1 - w0) * R_OCT;
     const int nj = tid < nq ? (nq - tid + kNT - 1) / kNT : 0;
@@ -596,7 +662,7 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
 #pragma unroll
     for (int j = 0; j < AP; ++j)
       apre[j] = j < nj ? ldg16(ap + (int64_t)j * kNT * 8) : make_uint4(0, 0, 0, 0);
-    if (prefetch && w0 == 0) {
+    if (prefetch && w0 == t.k0) {
       prefetch_b<bp_depth<TG>()>(g, t, bpre);
       prefetch_y<TG>(g, t, sm.tok, ypre);
     }
@@ -703,12 +769,13 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
                                             const uint4 (&bpre)[bp_depth<TG>()],
                                             const uint4 (&ypre)[TG], bool have_y) {
   constexpr int BP = bp_depth<TG>();
-  const ExpandMap m = expand_map(g, t);
-  const int n_oct = g.h_out >> 3;
+  const ExpandMap m = expand_map(t);
+  const int n_oct = m.n_oct;
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
   for (int cb = 0, co = m.co0; cb * kW * m.CPW < n_oct; ++cb, co += kW * m.CPW) {
     const bool col_ok = co < n_oct;
-    const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + (int64_t)co * 8;
+    const int jc = t.j0 + co * 8;                    // first y column of the octet
+    const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + jc;
     float d[TG * 8];
 #pragma unroll
     for (int i = 0; i < TG * 8; ++i) d[i] = 0.f;
@@ -738,7 +805,7 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
       for (int tt = 0; tt < TG; ++tt) {
         const int tk = tt < t.L ? sm.tok[tt] : -1;
         yv[tt] = (have_y && cb == 0) ? ypre[tt]
-                 : (tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + (int64_t)co * 8)
+                 : (tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + jc)
                             : make_uint4(0, 0, 0, 0));
       }
 #pragma unroll
@@ -755,7 +822,7 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
           out.y = ob[2] | (ob[3] << 16);
           out.z = ob[4] | (ob[5] << 16);
           out.w = ob[6] | (ob[7] << 16);
-          *reinterpret_cast<uint4*>(g.y + (int64_t)tk * g.ldy + (int64_t)co * 8) = out;
+          *reinterpret_cast<uint4*>(g.y + (int64_t)tk * g.ldy + jc) = out;
         }
       }
     }
@@ -820,10 +887,11 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
   const int r = t.r;
   const int S = r < 16 ? 16 : r;                   // LDS row stride of A_i chunks
   const int RK = rk_max(g.max_rank);
-  // rows per chunk: a multiple of kRK * kW, at most kChunk / S, and at most
-  // 4 K steps of x operands per wave over all M tiles
-  const int KC = min(kChunk / S, 1024 / MT);
-  const int nchunks = (g.h_in + KC - 1) / KC;
+  // rows per chunk: a multiple of kRK, at most kChunk / S, and at most XK
+  // K steps per wave
+  constexpr int XK = 4 / MT;
+  const int KC = min(kChunk / S, XK * kW * kRK);
+  const int nchunks = (t.k1 - t.k0 + KC - 1) / KC;
   uint16_t* As = sm.buf;
 
   f32x4_t acc[MT][NTN];
@@ -833,7 +901,6 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
     for (int nt = 0; nt < NTN; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // x operands of this wave's K steps of one chunk: [step][M tile]
-  constexpr int XK = 4 / MT;
   uint4 xcur[XK][MT], xnxt[XK][MT], areg[8];
   const int grp = lane >> 4;
   int toks[MT];
@@ -848,13 +915,13 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
       const int k = k0 + (w + i * kW) * kRK + 8 * grp;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
-        xo[i][mt] = (toks[mt] >= 0 && k < g.h_in && k < k0 + KC)
+        xo[i][mt] = (toks[mt] >= 0 && k < t.k1 && k < k0 + KC)
                         ? ldg16(g.x + (int64_t)toks[mt] * g.ldx + k)
                         : make_uint4(0, 0, 0, 0);
     }
   };
   auto load_a = [&](int k0) {
-    const int rows = min(KC, g.h_in - k0);
+    const int rows = min(KC, t.k1 - k0);
     const int n16 = rows * (r >> 3);
     const uint16_t* src = t.Ai + (int64_t)k0 * r;
 #pragma unroll
@@ -864,7 +931,7 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
     }
   };
   auto store_a = [&](int k0) {
-    const int rows = min(KC, g.h_in - k0);
+    const int rows = min(KC, t.k1 - k0);
     const int n16 = rows * (r >> 3);
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -884,17 +951,17 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
       *reinterpret_cast<uint4*>(As + rows * S + q * 8) = make_uint4(0, 0, 0, 0);
   };
 
-  load_x(0, xcur);
-  load_a(0);
+  load_x(t.k0, xcur);
+  load_a(t.k0);
   for (int c = 0; c < nchunks; ++c) {
-    const int k0 = c * KC;
+    const int k0 = t.k0 + c * KC;
     store_a(k0);
     lds_sync();
     if (c + 1 < nchunks) {
       load_x(k0 + KC, xnxt);
       load_a(k0 + KC);
     }
-    const int ksn = (min(KC, g.h_in - k0) + kRK - 1) / kRK;
+    const int ksn = (min(KC, t.k1 - k0) + kRK - 1) / kRK;
 #pragma unroll
     for (int i = 0; i < XK; ++i) {
       const int ks = w + i * kW;
@@ -978,8 +1045,8 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
   const int r = t.r;
   const int RK = rk_max(g.max_rank);
   const int rk = r < kRK ? kRK : r;                // K extent, zero rows above r
-  const int JC = min(kChunk / rk, (g.h_out + 15) / 16 * 16);   // columns per chunk
-  const int nchunks = (g.h_out + JC - 1) / JC;
+  const int JC = min(kChunk / rk, (t.j1 - t.j0 + 15) / 16 * 16);   // columns per chunk
+  const int nchunks = (t.j1 - t.j0 + JC - 1) / JC;
   uint16_t* Bs = sm.buf;
   const uint16_t* vhi = sm.vhl;
   const uint16_t* vlo = sm.vhl + kTT * RK;
@@ -993,7 +1060,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     toks[nt] = ti < t.L ? sm.tok[ti] : -1;
   }
   auto load_b = [&](int j0) {
-    const int cols = min(JC, g.h_out - j0);
+    const int cols = min(JC, t.j1 - j0);
     const int per_row = cols >> 3;
     const int n16 = r * per_row;
 #pragma unroll
@@ -1008,7 +1075,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     }
   };
   auto store_b = [&](int j0) {
-    const int cols = min(JC, g.h_out - j0);
+    const int cols = min(JC, t.j1 - j0);
     const int per_row = cols >> 3;
     const int n16 = r * per_row;
     const int S = (cols + 15) / 16 * 16;
@@ -1028,10 +1095,10 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       *reinterpret_cast<uint4*>(Bs + r * S + q * 8) = make_uint4(0, 0, 0, 0);
   };
 
-  load_b(0);
+  load_b(t.j0);
   for (int ch = 0; ch < nchunks; ++ch) {
-    const int j0 = ch * JC;
-    const int cols = min(JC, g.h_out - j0);
+    const int j0 = t.j0 + ch * JC;
+    const int cols = min(JC, t.j1 - j0);
     const int S = (cols + 15) / 16 * 16;
     const int njt = S / 16;
     store_b(j0);
@@ -1043,7 +1110,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       const int j = j0 + jt * 16 + 4 * grp;
 #pragma unroll
       for (int nt = 0; nt < MT; ++nt)
-        yv[i][nt] = (jt < njt && j < g.h_out && toks[nt] >= 0)
+        yv[i][nt] = (jt < njt && j < t.j1 && toks[nt] >= 0)
                         ? *reinterpret_cast<const uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j)
                         : make_uint2(0, 0);
     }
@@ -1069,7 +1136,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
         const int j = j0 + jt * 16 + 4 * grp;
 #pragma unroll
         for (int nt = 0; nt < MT; ++nt) {
-          if (toks[nt] >= 0 && j < g.h_out) {
+          if (toks[nt] >= 0 && j < t.j1) {
             const uint2 yw = yv[i][nt];
             const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
             const uint32_t o0 = to_bf16(fmaf(t.s, acc[nt][0], y0));
@@ -1140,11 +1207,13 @@ __device__ __forceinline__ Smem tile_prologue(const ApplyArgs& g, int my_tok, vo
 // kernels
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(kNT) void shrink_kernel(ApplyArgs g) {
+// plora_shrink: one item per tile; v of each valid token to g.v.
+__global__ __launch_bounds__(kNT, kWGPerCU) void shrink_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
+  const Plan p = make_plan(g, false);
   Tile t;
   int my_tok;
-  if (!load_tile(g, t, my_tok)) return;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
   tile_dispatch(g, t, sm, true, false);
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
@@ -1154,11 +1223,13 @@ __global__ __launch_bounds__(kNT) void shrink_kernel(ApplyArgs g) {
   }
 }
 
-__global__ __launch_bounds__(kNT) void expand_kernel(ApplyArgs g) {
+// plora_expand: the fused apply's items, with v read from g.v.
+__global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
+  const Plan p = make_plan(g, true);
   Tile t;
   int my_tok;
-  if (!load_tile(g, t, my_tok)) return;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
@@ -1169,11 +1240,13 @@ __global__ __launch_bounds__(kNT) void expand_kernel(ApplyArgs g) {
   tile_dispatch(g, t, sm, false, true);
 }
 
-__global__ __launch_bounds__(kNT) void apply_kernel(ApplyArgs g) {
+// plora_apply: the tile's shrink, then the expand of the item's slice.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
+  const Plan p = make_plan(g, true);
   Tile t;
   int my_tok;
-  if (!load_tile(g, t, my_tok)) return;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
   tile_dispatch(g, t, sm, true, true);
 }
@@ -1200,13 +1273,33 @@ inline bool usable_rank(int r, int max_rank) {
   return r == 0 || (r >= 8 && r <= max_rank && (r & (r - 1)) == 0);
 }
 
-// Expand row slots per column octet: the largest power of two that still
-// lets one work group cover every column octet of y in a single pass.
-int rsb_log2_for(int h_out) {
-  const int n_oct = h_out / 8;
-  int l = 0;
-  while (l < 6 && (n_oct << (l + 1)) <= kNT) ++l;
-  return l;
+// Compute units of the current device, queried once per device.
+int cu_count() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64) {
+    const int c = cache[dev].load();
+    if (c > 0) return c;
+  }
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0)
+    n = 256;
+  if (dev < 64) cache[dev].store(n);
+  return n;
+}
+
+// Resident work groups of the device: kWGPerCU per compute unit.
+int slots_for_device() { return std::max(8, cu_count() * kWGPerCU); }
+
+// One work group per item: the most items make_plan can produce for any tile
+// count up to tile_cap (see there).
+unsigned grid_for(const ApplyArgs& g, bool slices) {
+  const int64_t cap8 = (g.tile_cap + 7) & ~7;
+  if (!slices || g.js_max == 1) return (unsigned)std::max<int64_t>(8, cap8);
+  const int64_t spread = ((int64_t)g.slots * 4 / 3 + 8 + 7) & ~7;
+  return (unsigned)std::max<int64_t>(8, std::min(cap8 * g.js_max, std::max(cap8, spread)));
 }
 
 plora_status check_adapters_host(const plora_adapters* ad) {
@@ -1265,9 +1358,11 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   g.a_off = ad->a_off; g.b_off = ad->b_off; g.ranks = ad->ranks; g.scales = ad->scales;
   g.perm = seg->perm;
   g.tiles = reinterpret_cast<const int4*>(seg->tiles);
+  g.meta = seg->meta;
   g.T = seg->T; g.N = ad->n_adapters; g.h_in = ad->h_in; g.h_out = ad->h_out;
   g.max_rank = ad->max_rank; g.tile_cap = seg->tile_cap;
-  g.rsb_log2 = rsb_log2_for(ad->h_out);
+  g.js_max = std::max(1, ad->h_out / kMinSlice);
+  g.slots = slots_for_device();
   return PLORA_OK;
 }
 
@@ -1282,12 +1377,13 @@ void allow_lds(const void* kernel, std::atomic<bool>& done) {
 std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false};
 
 template <class K>
-plora_status launch_tiles(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
-                          hipStream_t stream) {
+plora_status launch_items(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
+                          bool slices, hipStream_t stream) {
   const size_t lds = smem_bytes(g.h_in, g.max_rank);
   if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(kernel), lds_done);
+  const unsigned grid = grid_for(g, slices);
   clear_stale_error();
-  hipLaunchKernelGGL(kernel, dim3((unsigned)g.tile_cap), dim3(kNT), lds, stream, g);
+  hipLaunchKernelGGL(kernel, dim3(grid), dim3(kNT), lds, stream, g);
   return launch_status();
 }
 
@@ -1353,7 +1449,7 @@ plora_status plora_shrink(const uint16_t* x, int64_t ldx, const plora_adapters* 
   if (ldx < ad->h_in || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldv & 3) || !aligned16(x) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.v = v; g.ldv = ldv;
-  return launch_tiles(shrink_kernel, g_lds_shrink, g, stream);
+  return launch_items(shrink_kernel, g_lds_shrink, g, false, stream);
 }
 
 plora_status plora_expand(const float* v, int64_t ldv, const plora_adapters* ad,
@@ -1367,7 +1463,7 @@ plora_status plora_expand(const float* v, int64_t ldv, const plora_adapters* ad,
   if (ldy < ad->h_out || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldy & 7) || (ldv & 3) || !aligned16(y) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.v = const_cast<float*>(v); g.ldv = ldv; g.y = y; g.ldy = ldy;
-  return launch_tiles(expand_kernel, g_lds_expand, g, stream);
+  return launch_items(expand_kernel, g_lds_expand, g, true, stream);
 }
 
 plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* ad,
@@ -1381,7 +1477,7 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
-  return launch_tiles(apply_kernel, g_lds_apply, g, stream);
+  return launch_items(apply_kernel, g_lds_apply, g, true, stream);
 }
 
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
