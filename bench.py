@@ -20,6 +20,7 @@ the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -30,6 +31,9 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
 MALL_BYTES = 256 << 20
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_05483_amd", "csrc", "plora.hip")
+PROFILES = os.path.join(ROOT, "profiles")
 
 
 def parse():
@@ -46,7 +50,49 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run 10 plain device copies of MIB MiB (the reference "
+                         "kernel for scaling HBM byte counters) and exit")
     return ap.parse_args()
+
+
+def source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(name: str):
+    """HBM bytes per apply launch from the committed counter summary of this
+    workload, or None when there is none or the kernel source has changed
+    since the counters were taken."""
+    path = os.path.join(PROFILES, f"plora_apply_{name}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        parts = line.split()
+        if len(parts) == 2 and parts[0].endswith(":"):
+            kv[parts[0][:-1]] = parts[1]
+    if kv.get("source_sha256") != source_digest():
+        return None
+    try:
+        return int(kv["fetch_bytes_per_launch"]) + int(kv["write_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib: int):
+    import torch
+    dev = torch.device("cuda:0")
+    n = mib << 20
+    src = torch.ones(n // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"bytes_read_per_copy": n,
+                                           "bytes_written_per_copy": n, "copies": 10}}),
+          flush=True)
 
 
 def describe(name, c):
@@ -63,9 +109,13 @@ def describe(name, c):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
-              "(the apply has no multi-GPU path in this build).", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the "
+              "apply runs on a single GPU (how it would shard is a design note only).",
+              file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration > 0:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
     from paper_2608_05483_amd import plora as P
@@ -140,6 +190,7 @@ def main():
     bytes_adapter = sum(ad_bytes[d] for d in ks)
     apply_s = apply_ms.sum() / 1e3
     achieved = bytes_total / apply_s / 1e9
+    traffic = measured_traffic(name)
     adapter_gbps = bytes_adapter / apply_s / 1e9
 
     # ---- same-footprint plain-read ceiling -------------------------------------
@@ -224,7 +275,7 @@ def main():
         "adapter_bytes_per_launch": int(bytes_adapter / K),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None},
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic},
         "read_ceiling": ceiling,
         "cpu_baseline": cpu,
     }

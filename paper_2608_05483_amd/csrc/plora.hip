@@ -2,9 +2,11 @@
 // adapter LoRA apply (declared in include/plora.h).
 //
 // What runs where:
-//   plora_segment  one 1024-thread work group: LSD radix sort of packed
-//                  (adapter id, token index) words in LDS, ballot-based stable
-//                  ranking per wavefront, then segment and tile lists.
+//   plora_segment  one work group.  Up to 1024 tokens: one thread per token
+//                  ranks its (adapter id, token index) key by counting the
+//                  keys before it in LDS.  Larger batches: LSD radix sort of
+//                  packed keys in LDS with ballot-based stable ranking per
+//                  wavefront.  Both then write the segment and tile lists.
 //   plora_shrink   persistent work groups (two per compute unit) striding
 //   plora_expand   over work items: one tile (PLORA_TILE_TOKENS tokens of one
 //   plora_apply    adapter, section VI-B's per-adapter batch B_i split into
@@ -55,12 +57,38 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
+// A 16-byte load of p where ok holds and of safe elsewhere, with zero in
+// place of the value there.  The load itself is unconditional: with a branch
+// around a load, the compiler waits for every load in flight where the
+// branches join instead of for the one it needs, and the vector path's
+// prefetching would be serialised.  Callers pick safe inside a line the same wavefront
+// reads anyway (the tile's first token row at the same column, the chunk
+// being loaded), so the masked lanes cost no extra traffic and no two work
+// groups pile onto one address.
+__device__ __forceinline__ uint4 ldg16z(const uint16_t* p, const uint16_t* safe, bool ok) {
+  const uint4 v = ldg16(ok ? p : safe);
+  return ok ? v : make_uint4(0, 0, 0, 0);
+}
+
+// The same with a branch around the load, for the matrix path: there, loads
+// are consumed chunk by chunk right after a barrier anyway, and the branch-free
+// form measured slower.
+__device__ __forceinline__ uint4 ldg16c(const uint16_t* p, bool ok) {
+  return ok ? ldg16(p) : make_uint4(0, 0, 0, 0);
+}
+
+__device__ __forceinline__ uint2 ldg8c(const uint16_t* p, bool ok) {
+  return ok ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+}
+
 // ---------------------------------------------------------------------------
 // plora_segment: stable grouping of tokens by adapter id
 // ---------------------------------------------------------------------------
 
-// Exclusive scan of one int per thread over the 1024-thread block.
-__device__ int block_exscan(int v, int* total, int* sh /* [kSegWaves + 1] */) {
+// Exclusive scan of one int per thread over a block of NW wavefronts.
+template <int NW = kSegWaves>
+__device__ int block_exscan(int v, int* total, int* sh /* [NW + 1] */) {
+  constexpr int kSegWaves = NW;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   int x = v;
 #pragma unroll
@@ -86,6 +114,93 @@ __device__ int block_exscan(int v, int* total, int* sh /* [kSegWaves + 1] */) {
   *total = sh[kSegWaves];
   __syncthreads();
   return res;
+}
+
+// Batches of T <= NT tokens, one thread per token.  Token t's key is its
+// adapter id, N for skipped tokens; its position in the grouping is the
+// number of keys below it plus the number of equal keys of earlier tokens
+// (a stable sort by key, then token index).  Segment and tile starts are then
+// flagged per position and numbered by block scans.
+template <int NT>
+__global__ __launch_bounds__(NT) void segment_small_kernel(
+    const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t cap,
+    int32_t tile_cap, int32_t* __restrict__ perm, int32_t* __restrict__ seg_ptr,
+    int32_t* __restrict__ seg_id, int32_t* __restrict__ meta, int4* __restrict__ tiles) {
+  constexpr int NW = NT / 64;
+  __shared__ int32_t key_t[NT];       // key of token t
+  __shared__ int32_t key_p[NT];       // key at grouped position p
+  __shared__ int32_t start_s[NT + 1]; // segment starts, then n_valid
+  __shared__ int32_t scan_sh[NW + 1];
+  const int t = threadIdx.x;
+
+  int key = N + 1;                    // threads past T sort after everything
+  int none = 0, invalid = 0;
+  if (t < T) {
+    const int id = idx[t];
+    if (id >= 0 && id < N) {
+      key = id;
+    } else {
+      key = N;
+      none = id == -1;
+      invalid = !none;
+    }
+  }
+  key_t[t] = key;
+  const int n_none = __syncthreads_count(none);
+  const int n_invalid = __syncthreads_count(invalid);
+  const int n_valid = T - n_none - n_invalid;
+
+  if (t < T) {
+    int rank = 0;
+    for (int u = 0; u < T; ++u) {
+      const int k = key_t[u];
+      rank += (k < key || (k == key && u < t)) ? 1 : 0;
+    }
+    key_p[rank] = key;
+    perm[rank] = key < N ? t : -1;
+  }
+  __syncthreads();
+
+  // segments: position p starts one when its key differs from p - 1's
+  const int p = t;
+  const bool sflag = p < n_valid && (p == 0 || key_p[p - 1] != key_p[p]);
+  int n_seg;
+  const int sidx = block_exscan<NW>(sflag ? 1 : 0, &n_seg, scan_sh);
+  if (sflag) {
+    seg_ptr[sidx] = p;
+    seg_id[sidx] = key_p[p];
+    start_s[sidx] = p;
+  }
+  if (t == 0) start_s[n_seg] = n_valid;
+  __syncthreads();
+  for (int q = n_seg + t; q <= cap; q += NT) seg_ptr[q] = n_valid;
+  for (int q = n_seg + t; q < cap; q += NT) seg_id[q] = -1;
+
+  // tiles: a position starts one when it lies a multiple of kTT past its
+  // segment's start; sidx + sflag - 1 is the segment of position p
+  const int cur = sidx + (sflag ? 1 : 0) - 1;
+  bool tflag = false;
+  int start = 0, end = 0;
+  if (p < n_valid) {
+    start = start_s[cur];
+    end = start_s[cur + 1];
+    tflag = ((p - start) % kTT) == 0;
+  }
+  int n_tiles;
+  const int tu = block_exscan<NW>(tflag ? 1 : 0, &n_tiles, scan_sh);
+  if (tflag && tu < tile_cap) tiles[tu] = make_int4(key_p[p], p, min(kTT, end - p), cur);
+  n_tiles = min(n_tiles, tile_cap);
+  for (int u = n_tiles + t; u < tile_cap; u += NT) tiles[u] = make_int4(-1, 0, 0, -1);
+  if (t == 0) {
+    meta[0] = n_seg;
+    meta[1] = n_valid;
+    meta[2] = n_none;
+    meta[3] = n_invalid;
+    meta[4] = n_tiles;
+    meta[5] = 0;
+    meta[6] = 0;
+    meta[7] = 0;
+  }
 }
 
 // Words are (key << tbits) | t, key = adapter id or N for skipped tokens.
@@ -341,6 +456,9 @@ constexpr int kAP = 16;              // most A_i chunks per thread requested up 
 constexpr int kBP = 16;              // most B_i chunks per thread requested up front
 constexpr int kXW = 4096;            // x row window staged in LDS (vector path)
 constexpr int kChunk = 16384;        // bf16 elements per LDS staging chunk (32 KiB)
+constexpr int kWaveRing = 12288;     // bytes of LDS ring per wavefront (matrix shrink)
+constexpr int kBufElems = kW * kWaveRing / 2 + 16;   // slack for transposed reads past the end
+static_assert(kBufElems >= kChunk, "the LDS buffer also stages B_i chunks and the x window");
 constexpr int kRK = 32;              // MFMA K step
 constexpr int kMinSlice = 512;       // fewest y columns per work item (but h_out)
 
@@ -457,8 +575,8 @@ __device__ __forceinline__ void lds_sync() {
 //   tok   [kTT]              token index of each tile row, -1 if unusable
 //   vs    [max_rank][kTT]    v of the tile, fp32, column-major
 //   vhl   [2][kTT][RKmax]    v split into bf16 high and low parts, token-major
-//   buf   kChunk bf16        single-token path: x window and the cross-wave
-//                            partial sums; matrix path: A_i / B_i chunks and
+//   buf   kBufElems bf16     vector path: x window and the cross-wave partial
+//                            sums; matrix path: the A_i ring, B_i chunks and
 //                            the wave-tree partial tiles
 struct Smem {
   int* tok;
@@ -474,7 +592,7 @@ __host__ __device__ constexpr int rk_max(int max_rank) {
 __host__ __device__ constexpr size_t smem_bytes(int h_in, int max_rank) {
   return kTT * sizeof(int) + (size_t)max_rank * kTT * sizeof(float) +
          (size_t)2 * kTT * rk_max(max_rank) * sizeof(uint16_t) +
-         (size_t)kChunk * sizeof(uint16_t) + 0 * h_in;
+         (size_t)kBufElems * sizeof(uint16_t) + 0 * h_in;
 }
 
 __device__ __forceinline__ Smem carve(void* base, int max_rank) {
@@ -531,7 +649,7 @@ __device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, ui
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
 #pragma unroll
   for (int j = 0; j < BP; ++j)
-    bpre[j] = (col_ok && j < m.njb) ? ldg16(bp + j * bstep) : make_uint4(0, 0, 0, 0);
+    bpre[j] = ldg16z(bp + j * bstep, t.Bi + t.j0, col_ok && j < m.njb);
 }
 
 // This thread's y words (first column octet, row slot 0) of the tile's tokens.
@@ -540,11 +658,11 @@ __device__ __forceinline__ void prefetch_y(const ApplyArgs& g, const Tile& t, co
                                            uint4 (&ypre)[TG]) {
   const ExpandMap m = expand_map(t);
   const bool ok = m.co0 < m.n_oct && m.rb == 0;
+  const uint16_t* safe = g.y + (int64_t)max(tok[0], 0) * g.ldy + t.j0;
 #pragma unroll
   for (int tt = 0; tt < TG; ++tt) {
     const int tk = (ok && tt < t.L) ? tok[tt] : -1;
-    ypre[tt] = tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + t.j0 + (int64_t)m.co0 * 8)
-                       : make_uint4(0, 0, 0, 0);
+    ypre[tt] = ldg16z(g.y + (int64_t)tk * g.ldy + t.j0 + (int64_t)m.co0 * 8, safe, tk >= 0);
   }
 }
 
@@ -649,19 +767,22 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
     const int q0 = w0 * R_OCT;                         // first chunk of the window
     const int nq = (w1 - w0) * R_OCT;
     const int nj = tid < nq ? (nq - tid + kNT - 1) / kNT : 0;
+    const int nj_max = (nq + kNT - 1) / kNT;       // the same for the whole group
     const int n8 = (w1 - w0) >> 3;                     // x chunks per token
     const uint16_t* ap = t.Ai + ((int64_t)q0 + tid) * 8;
+    const uint16_t* a_safe = t.Ai + (int64_t)q0 * 8;
+    const uint16_t* x_safe = g.x + (int64_t)max(sm.tok[0], 0) * g.ldx + w0;
     uint4 xr[XR], apre[AP];
 #pragma unroll
     for (int i = 0; i < XR; ++i) {
       const int c = tid + i * kNT;
       const int tt = c / n8, kc = c - tt * n8;
       const int tk = (tt < t.L && c < TG * n8) ? sm.tok[tt] : -1;
-      xr[i] = tk >= 0 ? ldg16(g.x + (int64_t)tk * g.ldx + w0 + kc * 8) : make_uint4(0, 0, 0, 0);
+      xr[i] = ldg16z(g.x + (int64_t)tk * g.ldx + w0 + kc * 8, x_safe, tk >= 0);
     }
 #pragma unroll
     for (int j = 0; j < AP; ++j)
-      apre[j] = j < nj ? ldg16(ap + (int64_t)j * kNT * 8) : make_uint4(0, 0, 0, 0);
+      apre[j] = ldg16z(ap + (int64_t)j * kNT * 8, a_safe, j < nj);
     if (prefetch && w0 == t.k0) {
       prefetch_b<bp_depth<TG>()>(g, t, bpre);
       prefetch_y<TG>(g, t, sm.tok, ypre);
@@ -680,23 +801,24 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
       }
     }
     lds_sync();
+    // the next batch is requested before the prefetched chunks are consumed,
+    // so that two batches are always in flight
+    uint4 a0[kCH], a1[kCH];
+#pragma unroll
+    for (int j = 0; j < kCH; ++j)
+      a0[j] = ldg16z(ap + (int64_t)(AP + j) * kNT * 8, a_safe, AP + j < nj);
 #pragma unroll
     for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
-    if (nj > AP) {
-      uint4 a0[kCH], a1[kCH];
-#pragma unroll
-      for (int j = 0; j < kCH; ++j)
-        a0[j] = (AP + j < nj) ? ldg16(ap + (int64_t)(AP + j) * kNT * 8) : make_uint4(0, 0, 0, 0);
-      for (int jb = AP; jb < nj; jb += 2 * kCH) {
+    if (nj_max > AP) {
+      for (int jb = AP; jb < nj_max; jb += 2 * kCH) {
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          a1[j] = (jb + kCH + j < nj) ? ldg16(ap + (int64_t)(jb + kCH + j) * kNT * 8)
-                                      : make_uint4(0, 0, 0, 0);
+          a1[j] = ldg16z(ap + (int64_t)(jb + kCH + j) * kNT * 8, a_safe, jb + kCH + j < nj);
         fma_a<R_OCT, TG>(val, a0, xs, q0, w0, jb, nj);
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          a0[j] = (jb + 2 * kCH + j < nj) ? ldg16(ap + (int64_t)(jb + 2 * kCH + j) * kNT * 8)
-                                          : make_uint4(0, 0, 0, 0);
+          a0[j] = ldg16z(ap + (int64_t)(jb + 2 * kCH + j) * kNT * 8, a_safe,
+                         jb + 2 * kCH + j < nj);
         fma_a<R_OCT, TG>(val, a1, xs, q0, w0, jb + kCH, nj);
       }
     }
@@ -790,7 +912,7 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
         uint4 b[kCH];
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          b[j] = (jb + j < m.njb) ? ldg16(bp + (int64_t)(jb + j) * bstep) : make_uint4(0, 0, 0, 0);
+          b[j] = ldg16z(bp + (int64_t)(jb + j) * bstep, t.Bi + jc, jb + j < m.njb);
         fma_b<TG>(d, b, sm, m, jb);
       }
     }
@@ -805,8 +927,8 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
       for (int tt = 0; tt < TG; ++tt) {
         const int tk = tt < t.L ? sm.tok[tt] : -1;
         yv[tt] = (have_y && cb == 0) ? ypre[tt]
-                 : (tk >= 0 ? ldg16(g.y + (int64_t)tk * g.ldy + jc)
-                            : make_uint4(0, 0, 0, 0));
+                 : ldg16z(g.y + (int64_t)tk * g.ldy + jc,
+                          g.y + (int64_t)max(sm.tok[0], 0) * g.ldy + jc, tk >= 0);
       }
 #pragma unroll
       for (int tt = 0; tt < TG; ++tt) {
@@ -878,21 +1000,77 @@ __device__ __forceinline__ bf16x8_t tr_operand(const uint16_t* m, int S, int rba
   return as_bf16x8(make_uint4(a.x, a.y, b.x, b.y));
 }
 
-// Shrink of a multi-token tile: MT M tiles of 16 tokens, NTN N tiles of 16
-// columns (r = 8 uses the first half of one tile).  Writes v to sm.vs (fp32)
-// and its high/low bf16 split to sm.vhl.
-template <int MT, int NTN>
+// s_waitcnt that waits until at most n vector-memory operations of this
+// wavefront are outstanding, leaving the other counters alone (gfx9
+// encoding: vmcnt bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// LDS address (byte offset in the work group's LDS) of a pointer into it.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)p;
+}
+
+// Reads of the shrink's LDS ring, issued as inline assembly.  The ring is
+// filled by global_load_lds, and the compiler, which cannot tell ring stages
+// apart, would make every LDS read it sees wait for every such load in flight
+// (s_waitcnt vmcnt(0)), serialising the ring; these reads are ordered by the
+// explicit waits of the ring instead.  Results are valid only after
+// lds_wait() has taken them.
+__device__ __forceinline__ uint64_t lds_tr16_b64(uint32_t a) {
+  uint64_t v;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  return v;
+}
+__device__ __forceinline__ u32x4_t lds_b128(uint32_t a) {
+  u32x4_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  return v;
+}
+
+// Shrink of a tile of more than kVT tokens on the matrix cores, for rank R:
+// MT M tiles of 16 tokens, NTN N tiles of 16 columns (R = 8 uses the first
+// half of one; its other columns are read past the row end and never
+// stored).  Wavefront w takes the K steps (32 rows of h_in) w, w + kW, ...,
+// in stages of KW steps, and streams each stage's rows of A_i and its x
+// operands straight from global memory into a ring of D stages of its own
+// LDS (global_load_lds_dwordx4, no registers), D stages ahead of its matrix
+// cores; no wavefront waits for another until the final reduction.  Every
+// stage issues the same loads (a stage past the wavefront's last re-reads its
+// last, loads past the block re-read the stage's start), so the loads in
+// flight behind a stage are a constant number and the wait for it is exact.
+// Rows of the last K step past the block are zeroed in LDS before use.
+// Writes v to sm.vs (fp32) and its high/low bf16 split to sm.vhl.
+template <int MT, int R>
 __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int r = t.r;
-  const int S = r < 16 ? 16 : r;                   // LDS row stride of A_i chunks
+  constexpr int NTN = R < 16 ? 1 : R / 16;
+  constexpr int KW = R < 16 ? 2 : 1;                  // K steps per stage
+  constexpr int SR = KW * kRK;                        // rows of h_in per stage
+  constexpr int AB = SR * R * 2;                      // bytes of A_i per stage
+  constexpr int XB = SR * MT * 16 * 2;                // bytes of x per stage
+  constexpr int NAI = AB / 1024, NXI = XB / 1024;     // loads per lane per stage
+  constexpr int STG = AB + XB;
+  constexpr int D = kWaveRing / STG < 1 ? 1 : (kWaveRing / STG > 8 ? 8 : kWaveRing / STG);
+  constexpr int XU = 16 * MT;                         // x units (16 bytes) per 8 columns
+  static_assert(NAI * 1024 == AB && NXI * 1024 == XB, "stages are whole loads");
+  static_assert(D * STG <= kWaveRing, "the ring fits");
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4, lp = lane & 15;
   const int RK = rk_max(g.max_rank);
-  // rows per chunk: a multiple of kRK, at most kChunk / S, and at most XK
-  // K steps per wave
-  constexpr int XK = 4 / MT;
-  const int KC = min(kChunk / S, XK * kW * kRK);
-  const int nchunks = (t.k1 - t.k0 + KC - 1) / KC;
-  uint16_t* As = sm.buf;
+  const int nst = (t.k1 - t.k0 + SR - 1) / SR;        // stages over the block
+  const int my_n = w < nst ? (nst - w + kW - 1) / kW : 0;
+  char* ring = reinterpret_cast<char*>(sm.buf) + w * kWaveRing;
+
+  // x row this lane loads: tile row lane % XU (the tile's first token's row
+  // where that row holds no token; its products land in rows never stored)
+  const int xr = lane % XU;
+  const int xtok = xr < t.L ? sm.tok[xr] : -1;
+  const uint16_t* x_row0 = g.x + (int64_t)max(sm.tok[0], 0) * g.ldx;
+  const uint16_t* x_mine = xtok >= 0 ? g.x + (int64_t)xtok * g.ldx : x_row0;
 
   f32x4_t acc[MT][NTN];
 #pragma unroll
@@ -900,88 +1078,89 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
 #pragma unroll
     for (int nt = 0; nt < NTN; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // x operands of this wave's K steps of one chunk: [step][M tile]
-  uint4 xcur[XK][MT], xnxt[XK][MT], areg[8];
-  const int grp = lane >> 4;
-  int toks[MT];
+  // this wavefront's stage j into ring slot sl
+  auto issue = [&](int j, int sl) {
+    const int st = w + min(j, my_n - 1) * kW;
+    const int kr0 = t.k0 + st * SR;
+    const int n16 = min(SR, t.k1 - kr0) * (R / 8);    // valid 16-byte units of A_i
+    const uint16_t* asrc = t.Ai + (int64_t)kr0 * R;
+    char* base = ring + sl * STG;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int ti = mt * 16 + (lane & 15);
-    toks[mt] = ti < t.L ? sm.tok[ti] : -1;
-  }
-  auto load_x = [&](int k0, uint4 (&xo)[XK][MT]) {
-#pragma unroll
-    for (int i = 0; i < XK; ++i) {
-      const int k = k0 + (w + i * kW) * kRK + 8 * grp;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-        xo[i][mt] = (toks[mt] >= 0 && k < t.k1 && k < k0 + KC)
-                        ? ldg16(g.x + (int64_t)toks[mt] * g.ldx + k)
-                        : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < NAI; ++i) {
+      const int u = 64 * i + lane;
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(asrc + (u < n16 ? u : 0) * 8),
+          (__attribute__((address_space(3))) void*)(base + 64 * i * 16), 16, 0, 0);
     }
+#pragma unroll
+    for (int i = 0; i < NXI; ++i) {
+      const int k = kr0 + ((64 * i + lane) / XU) * 8;
+      const uint16_t* src = k < t.k1 ? x_mine + k : x_row0 + t.k0;
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)src,
+          (__attribute__((address_space(3))) void*)(base + AB + 64 * i * 16), 16, 0, 0);
+    }
+    // keep every load of this stage above the waits that count it
+    asm volatile("" ::: "memory");
   };
-  auto load_a = [&](int k0) {
-    const int rows = min(KC, t.k1 - k0);
-    const int n16 = rows * (r >> 3);
-    const uint16_t* src = t.Ai + (int64_t)k0 * r;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int q = tid + j * kNT;
-      areg[j] = q < n16 ? ldg16(src + (int64_t)q * 8) : make_uint4(0, 0, 0, 0);
+  auto consume = [&](int j, int sl) {
+    wait_vm<(D - 1) * (NAI + NXI)>();
+    const int st = w + j * kW;
+    const int rows = min(SR, t.k1 - t.k0 - st * SR);
+    char* base = ring + sl * STG;
+    if (rows < SR) {
+      // the block ends inside this stage: zero the rows past it and their x
+      for (int o = lane; o < (SR - rows) * (R / 8); o += 64)
+        reinterpret_cast<uint4*>(base + rows * R * 2)[o] = make_uint4(0, 0, 0, 0);
+      for (int o = lane; o < (SR - rows) / 8 * XU; o += 64)
+        reinterpret_cast<uint4*>(base + AB + rows / 8 * XU * 16)[o] = make_uint4(0, 0, 0, 0);
     }
-  };
-  auto store_a = [&](int k0) {
-    const int rows = min(KC, t.k1 - k0);
-    const int n16 = rows * (r >> 3);
+    const uint32_t a0 = lds_addr(base);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int q = tid + j * kNT;
-      if (q < n16) {
-        if (r == 8) {
-          *reinterpret_cast<uint4*>(As + q * 16) = areg[j];
-          *reinterpret_cast<uint4*>(As + q * 16 + 8) = make_uint4(0, 0, 0, 0);
-        } else {
-          *reinterpret_cast<uint4*>(As + q * 8) = areg[j];
-        }
-      }
-    }
-    // zero the rows that pad the last K step of the chunk
-    const int padded = (rows + kRK - 1) / kRK * kRK;
-    for (int q = tid; q < (padded - rows) * (S >> 3); q += kNT)
-      *reinterpret_cast<uint4*>(As + rows * S + q * 8) = make_uint4(0, 0, 0, 0);
-  };
-
-  load_x(t.k0, xcur);
-  load_a(t.k0);
-  for (int c = 0; c < nchunks; ++c) {
-    const int k0 = t.k0 + c * KC;
-    store_a(k0);
-    lds_sync();
-    if (c + 1 < nchunks) {
-      load_x(k0 + KC, xnxt);
-      load_a(k0 + KC);
-    }
-    const int ksn = (min(KC, t.k1 - k0) + kRK - 1) / kRK;
-#pragma unroll
-    for (int i = 0; i < XK; ++i) {
-      const int ks = w + i * kW;
-      if (ks < ksn) {
+    for (int kk = 0; kk < KW; ++kk) {
+      if (kk * kRK < rows) {
+        uint64_t bt[NTN][2];
+        u32x4_t xa[MT];
 #pragma unroll
         for (int nt = 0; nt < NTN; ++nt) {
-          const bf16x8_t b = tr_operand(As, S, ks * kRK, nt * 16);
+          const uint32_t ad =
+              a0 + ((kk * kRK + 8 * grp + (lp >> 2)) * R + nt * 16 + 4 * (lp & 3)) * 2;
+          bt[nt][0] = lds_tr16_b64(ad);
+          bt[nt][1] = lds_tr16_b64(ad + 4 * R * 2);
+        }
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(xcur[i][mt]), b,
-                                                                  acc[mt][nt], 0, 0, 0);
+        for (int mt = 0; mt < MT; ++mt)
+          xa[mt] = lds_b128(a0 + AB + ((kk * 4 + grp) * XU + mt * 16 + lp) * 16);
+        // the reads above complete before their registers are used
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int nt = 0; nt < NTN; ++nt) {
+          asm volatile("" : "+v"(bt[nt][0]), "+v"(bt[nt][1]));
+          const uint2 lo = __builtin_bit_cast(uint2, bt[nt][0]);
+          const uint2 hi = __builtin_bit_cast(uint2, bt[nt][1]);
+          const bf16x8_t b = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            asm volatile("" : "+v"(xa[mt]));
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8_t, xa[mt]), b, acc[mt][nt], 0, 0, 0);
+          }
         }
       }
     }
-    lds_sync();
+    issue(j + D, sl);
+  };
+  if (my_n > 0) {
 #pragma unroll
-    for (int i = 0; i < XK; ++i)
+    for (int sl = 0; sl < D; ++sl) issue(sl, sl);
+    for (int j0 = 0; j0 < my_n; j0 += D) {
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) xcur[i][mt] = xnxt[i][mt];
+      for (int sl = 0; sl < D; ++sl)
+        if (j0 + sl < my_n) consume(j0 + sl, sl);
+    }
   }
+  wait_vm<0>();                                     // the ring's last re-reads
+  lds_sync();
 
   // pairwise tree over the wavefronts: 4 -> 2 -> 1 slots, fixed order
   f32x4_t* slot = reinterpret_cast<f32x4_t*>(sm.buf);
@@ -1012,14 +1191,14 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
       for (int nt = 0; nt < NTN; ++nt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int tt = mt * 16 + 4 * grp + i, c = nt * 16 + (lane & 15);
-          if (tt < t.L && c < r) {
+          const int tt = mt * 16 + 4 * grp + i, cidx = nt * 16 + lp;
+          if (tt < t.L && cidx < R) {
             const float val = acc[mt][nt][i];
             const uint32_t hb = to_bf16(val);
             const float hv = __uint_as_float(hb << 16);
-            sm.vs[c * kTT + tt] = val;
-            vhi[tt * RK + c] = (uint16_t)hb;
-            vlo[tt * RK + c] = (uint16_t)to_bf16(val - hv);
+            sm.vs[cidx * kTT + tt] = val;
+            vhi[tt * RK + cidx] = (uint16_t)hb;
+            vlo[tt * RK + cidx] = (uint16_t)to_bf16(val - hv);
           }
         }
   }
@@ -1066,12 +1245,8 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int q = tid + j * kNT;
-      if (q < n16) {
-        const int c = q / per_row, col = q - c * per_row;
-        breg[j] = ldg16(t.Bi + (int64_t)c * g.h_out + j0 + col * 8);
-      } else {
-        breg[j] = make_uint4(0, 0, 0, 0);
-      }
+      const int c = q / per_row, col = q - c * per_row;
+      breg[j] = ldg16c(t.Bi + (int64_t)c * g.h_out + j0 + col * 8, q < n16);
     }
   };
   auto store_b = [&](int j0) {
@@ -1108,11 +1283,10 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     for (int i = 0; i < JT; ++i) {
       const int jt = w + i * kW;
       const int j = j0 + jt * 16 + 4 * grp;
+      const bool jok = jt < njt && j < t.j1;
 #pragma unroll
       for (int nt = 0; nt < MT; ++nt)
-        yv[i][nt] = (jt < njt && j < t.j1 && toks[nt] >= 0)
-                        ? *reinterpret_cast<const uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j)
-                        : make_uint2(0, 0);
+        yv[i][nt] = ldg8c(g.y + (int64_t)toks[nt] * g.ldy + j, jok && toks[nt] >= 0);
     }
     if (ch + 1 < nchunks) load_b(j0 + JC);
 #pragma unroll
@@ -1161,20 +1335,21 @@ __device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, con
   lds_sync();
   const bool two = t.L > 16;
   if (do_shrink) {
-    const int ntn = t.r <= 16 ? 1 : t.r / 16;
     if (two) {
-      switch (ntn) {
-        case 1: shrink_mfma<2, 1>(g, t, sm); break;
-        case 2: shrink_mfma<2, 2>(g, t, sm); break;
-        case 4: shrink_mfma<2, 4>(g, t, sm); break;
-        default: shrink_mfma<2, 8>(g, t, sm); break;
+      switch (t.r) {
+        case 8: shrink_mfma<2, 8>(g, t, sm); break;
+        case 16: shrink_mfma<2, 16>(g, t, sm); break;
+        case 32: shrink_mfma<2, 32>(g, t, sm); break;
+        case 64: shrink_mfma<2, 64>(g, t, sm); break;
+        default: shrink_mfma<2, 128>(g, t, sm); break;
       }
     } else {
-      switch (ntn) {
-        case 1: shrink_mfma<1, 1>(g, t, sm); break;
-        case 2: shrink_mfma<1, 2>(g, t, sm); break;
-        case 4: shrink_mfma<1, 4>(g, t, sm); break;
-        default: shrink_mfma<1, 8>(g, t, sm); break;
+      switch (t.r) {
+        case 8: shrink_mfma<1, 8>(g, t, sm); break;
+        case 16: shrink_mfma<1, 16>(g, t, sm); break;
+        case 32: shrink_mfma<1, 32>(g, t, sm); break;
+        case 64: shrink_mfma<1, 64>(g, t, sm); break;
+        default: shrink_mfma<1, 128>(g, t, sm); break;
       }
     }
   } else {
@@ -1431,10 +1606,23 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg, int32_
   const int key_bits = n_adapters > 0 ? 32 - __builtin_clz((unsigned)n_adapters) : 0;
   if (tbits + key_bits > 32) return PLORA_ERR_UNSUPPORTED;
   clear_stale_error();
-  hipLaunchKernelGGL(segment_kernel, dim3(1), dim3(kSegThreads), 0, stream, idx, T,
-                     n_adapters, seg->cap, seg->tile_cap, tbits, key_bits, seg->perm,
-                     seg->seg_ptr, seg->seg_id, seg->meta,
-                     reinterpret_cast<int4*>(seg->tiles));
+  int4* tiles = reinterpret_cast<int4*>(seg->tiles);
+  if (T <= 64)
+    hipLaunchKernelGGL(segment_small_kernel<64>, dim3(1), dim3(64), 0, stream, idx, T,
+                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       seg->seg_id, seg->meta, tiles);
+  else if (T <= 256)
+    hipLaunchKernelGGL(segment_small_kernel<256>, dim3(1), dim3(256), 0, stream, idx, T,
+                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       seg->seg_id, seg->meta, tiles);
+  else if (T <= 1024)
+    hipLaunchKernelGGL(segment_small_kernel<1024>, dim3(1), dim3(1024), 0, stream, idx, T,
+                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       seg->seg_id, seg->meta, tiles);
+  else
+    hipLaunchKernelGGL(segment_kernel, dim3(1), dim3(kSegThreads), 0, stream, idx, T,
+                       n_adapters, seg->cap, seg->tile_cap, tbits, key_bits, seg->perm,
+                       seg->seg_ptr, seg->seg_id, seg->meta, tiles);
   return launch_status();
 }
 

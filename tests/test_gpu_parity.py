@@ -190,7 +190,11 @@ def _seg_inputs():
     for name in W.CONFIG_NAMES:
         cases.append((name, W.draw_idx(name, 1000 + W.CONFIG_NAMES.index(name)),
                       W.CONFIGS[name].N))
-    for T, N in [(16384, 1000), (16384, 7), (5000, 40000), (1023, 1024), (1025, 2)]:
+    # sizes at and around each segmentation kernel's limit (64, 256, 1024
+    # tokens), with skipped ids mixed in and segments longer than one tile
+    for T, N in [(2, 1), (63, 3), (64, 3), (65, 1000), (256, 2), (257, 50), (1024, 1),
+                 (1024, 1000), (16384, 1000), (16384, 7), (5000, 40000), (1023, 1024),
+                 (1025, 2)]:
         idx = rng.integers(-1, N, size=T).astype(np.int32)
         cases.append((f"rand_T{T}_N{N}", idx, N))
     cases.append(("zipf_max", W.zipf_ids(rng, 16384, 1000, 1.0), 1000))
