@@ -236,8 +236,9 @@ def main():
         import oracle
         cores = len(os.sched_getaffinity(0))
         n_done, toks, t_cpu = 0, 0, 0.0
-        while t_cpu < args.cpu_seconds and n_done < len(draws):
-            d = draws[n_done]
+        # cycle through the draws until the time budget is spent
+        while t_cpu < args.cpu_seconds:
+            d = draws[n_done % len(draws)]
             wd = w if d.size == w.T else W.with_idx(w, d)
             t1 = time.perf_counter()
             oracle.apply(wd.x, d, w.A, w.a_off, w.B, w.b_off, w.ranks, w.scales,
@@ -247,8 +248,9 @@ def main():
             n_done += 1
         cpu = {"value": round(toks / t_cpu, 1), "unit": "tokens/s", "cores": cores,
                "kind": "oracle",
-               "sample": f"{n_done} batches of this workload ({toks} tokens, "
-                         f"{t_cpu:.1f} s), fp32 C oracle, OpenMP over tokens"}
+               "sample": f"{n_done} batches of this workload, cycling its "
+                         f"{len(draws)} token draws ({toks} tokens, {t_cpu:.1f} s), "
+                         f"fp32 C oracle, OpenMP over tokens"}
 
     out = {
         "metric": "tokens/s and effective adapter GB/s (% of HBM peak) for plora_apply",

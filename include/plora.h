@@ -22,7 +22,9 @@
  *   plora_segment  group tokens by adapter id (stable counting sort)
  *   plora_shrink   v[t, :] = x[t, :] A_i            (E4's m = xA, fp32)
  *   plora_expand   y[t, :] += s_i v[t, :] B_i        (E4's y = mB)
- *   plora_apply    both in one launch; v never leaves the work group's LDS
+ *   plora_apply    both: one launch for batches of up to 1024 tokens (v
+ *                  stays on chip), two above (per-slice partial sums of v,
+ *                  fp32, pass through the workspace)
  *
  * Data types and layouts (all row-major, element strides):
  *   x       bf16 [T, ldx], first h_in columns used
@@ -37,9 +39,10 @@
  * plora_apply equals plora_shrink followed by plora_expand bit for bit.
  *
  * Memory and ownership: every pointer below is a DEVICE pointer unless the
- * text says "host"; the caller allocates and owns every buffer.  No call
- * allocates device memory, synchronizes the device or the stream, or keeps a
- * pointer after it returns (plora_check_adapters alone copies to the host and
+ * text says "host"; the caller allocates and owns every buffer, including
+ * the workspace (plora_workspace_bytes tells its size).  No call allocates
+ * device memory, synchronizes the device or the stream, or keeps a pointer
+ * after it returns (plora_check_adapters alone copies to the host and
  * waits).  Every launch goes onto the caller's stream.
  *
  * Errors: a call returns PLORA_OK or an error before launching anything,
@@ -54,7 +57,8 @@
  *                              T above PLORA_MAX_TOKENS; (N+1) * 2^ceil(log2 T)
  *                              beyond 2^32
  *   PLORA_ERR_WORKSPACE_TOO_SMALL  ws_bytes below plora_workspace_bytes()
- *                              (never, while that returns 0)
+ *                              where the call needs a workspace (a NULL ws
+ *                              there is PLORA_ERR_INVALID_ARG)
  *   PLORA_ERR_HIP              this call's launch failed (hipGetLastError;
  *                              an error left pending by earlier HIP calls
  *                              is cleared before launching)
@@ -163,13 +167,17 @@ typedef struct {
  * tiles a batch of T tokens over N adapters can produce; 0 for T <= 0. */
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 
-/* Host.  Bytes of device workspace the calls need for a batch of T tokens
- * over this adapter stack.  Every kernel of this version keeps its
- * intermediates in LDS, so this returns 0 and ws may be NULL everywhere; the
- * arguments stay in the ABI so that a later version can ask for scratch. */
+/* Host.  Bytes of device workspace plora_apply and plora_shrink need for a
+ * batch of up to T tokens over this adapter stack: the partial sums of v over
+ * up to 8 slices of h_in, fp32, K * T * max_rank * 4 bytes with
+ * K = min(8, max(1, h_in / 512)); 0 for T <= 0.  The workspace needs no
+ * initialisation (every partial is written before it is read) and holds
+ * nothing between calls; calls that share one must not overlap in time.
+ * plora_segment and plora_expand take none (ws may be NULL). */
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad);
 
-/* Zero a workspace (enqueued on stream; a no-op for ws_bytes == 0). */
+/* Zero a workspace (enqueued on stream; a no-op for ws_bytes == 0).  Not
+ * required by any call; for callers that want defined contents. */
 plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
@@ -185,7 +193,10 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg,
 /*
  * v[t, c] = sum_k x[t, k] * A_i[k, c] for every valid token t and c < r_i
  * (the rank-r reduction m = xA of strategy E4, section V-A).  Entries of v
- * for other tokens and columns are not written.
+ * for other tokens and columns are not written.  Two launches: the partial
+ * sums over slices of h_in into ws (at least plora_workspace_bytes(T) bytes,
+ * 16-byte aligned; one slice for T <= 1024), then their sum, in slice order,
+ * into v.
  */
 plora_status plora_shrink(const uint16_t* x, int64_t ldx,
                           const plora_adapters* ad, const plora_segments* seg,
@@ -202,9 +213,12 @@ plora_status plora_expand(const float* v, int64_t ldv,
                           hipStream_t stream);
 
 /*
- * The fused apply, one launch: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for
- * every valid token (strategy E1: both matrices resident in GPU memory,
- * section V-A).  x and y must not overlap.
+ * The apply: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for every valid token
+ * (strategy E1: both matrices resident in GPU memory, section V-A).  For
+ * T <= 1024 one launch; above, two launches with v's partial sums passed
+ * through ws.  ws must hold plora_workspace_bytes(T) bytes, 16-byte aligned,
+ * in both cases.  Bit for bit the same as plora_shrink followed by
+ * plora_expand.  x and y must not overlap.
  */
 plora_status plora_apply(const uint16_t* x, int64_t ldx,
                          const plora_adapters* ad, const plora_segments* seg,

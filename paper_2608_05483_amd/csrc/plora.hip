@@ -7,11 +7,12 @@
 //                  keys before it in LDS.  Larger batches: LSD radix sort of
 //                  packed keys in LDS with ballot-based stable ranking per
 //                  wavefront.  Both then write the segment and tile lists.
-//   plora_shrink   persistent work groups (two per compute unit) striding
-//   plora_expand   over work items: one tile (PLORA_TILE_TOKENS tokens of one
-//   plora_apply    adapter, section VI-B's per-adapter batch B_i split into
-//                  tiles) and one slice of the y columns; details above the
-//                  apply kernels below.
+//   plora_shrink   one work group per work item: one tile (up to
+//   plora_expand   PLORA_TILE_TOKENS tokens of one adapter, section VI-B's
+//   plora_apply    per-adapter batch B_i split into tiles) and one slice of
+//                  h_in or of the y columns; plora_apply is one launch for
+//                  batches of up to kFusedTokens tokens and two above;
+//                  details above the apply kernels below.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -225,18 +226,33 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   if (tid == 0) { n_none_sh = 0; n_invalid_sh = 0; }
   __syncthreads();
 
-  // load and pack; count skipped tokens
+  // load and pack; count skipped tokens.  Eight loads per thread are issued
+  // before any is used (addresses past T re-read idx[0]), so the batch costs
+  // one memory round trip per eight, not one per token.
   int my_none = 0, my_invalid = 0;
-  for (int t = tid; t < T; t += kSegThreads) {
-    int id = idx[t];
-    uint32_t key;
-    if (id >= 0 && id < N) {
-      key = (uint32_t)id;
-    } else {
-      key = (uint32_t)N;
-      if (id == -1) ++my_none; else ++my_invalid;
+  constexpr int kLoadBatch = 8;
+  for (int t0 = 0; t0 < T; t0 += kLoadBatch * kSegThreads) {
+    int ids[kLoadBatch];
+#pragma unroll
+    for (int j = 0; j < kLoadBatch; ++j) {
+      const int t = t0 + j * kSegThreads + tid;
+      ids[j] = idx[t < T ? t : 0];
     }
-    buf0[t] = (key << tbits) | (uint32_t)t;
+#pragma unroll
+    for (int j = 0; j < kLoadBatch; ++j) {
+      const int t = t0 + j * kSegThreads + tid;
+      if (t < T) {
+        const int id = ids[j];
+        uint32_t key;
+        if (id >= 0 && id < N) {
+          key = (uint32_t)id;
+        } else {
+          key = (uint32_t)N;
+          if (id == -1) ++my_none; else ++my_invalid;
+        }
+        buf0[t] = (key << tbits) | (uint32_t)t;
+      }
+    }
   }
   if (my_none) atomicAdd(&n_none_sh, my_none);
   if (my_invalid) atomicAdd(&n_invalid_sh, my_invalid);
@@ -404,22 +420,32 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // apply kernels
 // ---------------------------------------------------------------------------
 //
-// Work items.  An item is one tile and one slice of the y columns.  The
-// fused apply computes the tile's v = x A_i over all of h_in in each of its
-// items and expands it with that slice of B_i, so a tile's slices need no
-// communication.  A_i is then read by every slice of its tile: the items of
-// one tile are numbered so that they fall on work groups of one XCD (work
-// group b runs on XCD b mod 8), where the first read brings A_i into the
-// XCD's L2 and the others hit it.  The number of slices JS is chosen on the
-// device from the tile count the segmentation wrote, so that a decode batch
-// of a few dozen tiles still spreads over every compute unit, and each work
-// group takes one item; the grid is an upper bound on the item count that the
-// host derives from the tile capacity, and surplus work groups return at
-// once.
+// Work items.  An item is one tile and one slice of h_in (KS slices of KR
+// rows) or of the y columns (JS slices of W columns).  KS and JS are chosen
+// on the device from the tile count that plora_segment wrote, so that each
+// launch has about one item per resident work group (two per compute unit)
+// and a batch of a few dozen tiles still spreads over the whole chip; the
+// host sizes each grid to the most items any tile count can produce, and
+// surplus work groups return after one load.  Nothing passes between work
+// groups inside a launch: that would need agent-scope release and acquire,
+// an L2 write-back across XCDs on MI355X.  plora_apply takes one of two
+// forms, by batch size:
+//
+//   one launch (up to kFusedTokens tokens, decode batches): item (tile,
+//   column slice) computes the tile's v over all of h_in, then expands it
+//   with its slice of B_i.  A_i is read by every column slice of its tile;
+//   the slices of a tile are numbered onto one XCD, so the first read brings
+//   A_i into that XCD's L2 and the others hit it.  One launch boundary fewer
+//   is worth more than the repeated L2 reads when the batch is small.
+//
+//   two launches (larger batches, where x dominates): item (tile, h_in
+//   slice) writes its partial v to the workspace; item (tile, column slice)
+//   sums the tile's KS partials in slice order and expands.  Every byte of
+//   A_i, B_i and x is then read by one work group only.
 //
 // Two code paths, chosen per tile:
 //
-// Tiles of up to kVT tokens (vector ALU).  A_i, a contiguous block of h_in
+// Short tiles (vector ALU, see vector_tokens).  A_i, a contiguous block of h_in
 // x r bf16 values, is streamed as 16-byte chunks: thread tid loads chunks
 // tid, tid + kNT, ... so it always sees the column octet tid % (r/8) and a
 // set of rows, and accumulates x[row] * A_i[row][octet] in registers for
@@ -433,11 +459,12 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // in order).
 //
 // Longer tiles (matrix cores, v_mfma_f32_16x16x32_bf16).  The shrink
-// computes D[token][c] = sum_k x[token][k] A_i[k][c]: x rows feed the A
-// operand straight from global memory; A_i is staged in LDS in row chunks and
-// read back transposed (ds_read_b64_tr_b16) into the B operand.  Wavefronts
-// take interleaved 32-row K steps and their partial tiles are summed by a
-// fixed pairwise tree.  The expand computes D^T[j][token] =
+// computes D[token][c] = sum_k x[token][k] A_i[k][c]: each wavefront takes
+// every fourth 32-row K step and streams those rows of A_i and the x
+// operands straight into a ring of its own LDS stages (global_load_lds), the
+// x rows feeding the A operand and A_i read back transposed
+// (ds_read_b64_tr_b16) into the B operand; the four wavefronts' partial tiles
+// are summed by a fixed pairwise tree.  The expand computes D^T[j][token] =
 // sum_c B_i[c][j] v[token][c] with B_i column chunks staged in LDS and read
 // transposed into the A operand; v is split into bf16 high and low parts
 // (v = hi + lo to about 2^-17 relative) so that no intermediate is rounded
@@ -445,9 +472,10 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // token.
 //
 // Every reduction has a fixed order that depends only on the tile and the
-// slice width, so results are bitwise reproducible, and the split calls
-// (plora_shrink then plora_expand, which choose the same slices) run the very
-// same code on the very same values as the fused call.
+// slice widths, so results are bitwise reproducible, and the split calls
+// (plora_shrink, which sums the partials in the same order into v, then
+// plora_expand, which chooses the same column slices) compute the very same
+// values as plora_apply.
 
 constexpr int kNT = 256;             // threads per work group
 constexpr int kW = kNT / 64;         // wavefronts per work group
@@ -461,6 +489,7 @@ constexpr int kBufElems = kW * kWaveRing / 2 + 16;   // slack for transposed rea
 static_assert(kBufElems >= kChunk, "the LDS buffer also stages B_i chunks and the x window");
 constexpr int kRK = 32;              // MFMA K step
 constexpr int kMinSlice = 512;       // fewest y columns per work item (but h_out)
+constexpr int kFusedTokens = 1024;   // largest batch plora_apply runs as one launch
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -485,6 +514,8 @@ struct ApplyArgs {
   const int4* tiles;
   const int32_t* meta;
   int32_t T, N, h_in, h_out, max_rank, tile_cap;
+  float* vpart;         // workspace: partial v [ks_max][T][max_rank]
+  int32_t ks_max;      // most h_in slices per tile
   int32_t js_max;      // most y column slices per tile
   int32_t slots;       // resident work groups the device holds (item target)
 };
@@ -499,26 +530,36 @@ struct Tile {
   float s;
 };
 
-// The items of one launch: n_tiles tiles (as written by plora_segment),
-// rounded up to a multiple of 8, times JS column slices of W columns (a
-// multiple of 16, the last one shorter).  JS is the slot count over the
-// rounded tile count, to nearest, within [1, js_max]; so the item count is at
-// most max(4/3 slots, rounded tile count) and at most js_max times the
-// rounded tile count, whichever is less (the host sizes the grid by that).
+// The slices of one call: n_tiles tiles (as written by plora_segment),
+// rounded up to a multiple of 8, times KS slices of KR rows of h_in (a
+// multiple of 64, the last one shorter) for the shrink launch, or times JS
+// slices of W y columns (a multiple of 16, the last one shorter) for the
+// expand launch.  KS and JS are the slot count over the rounded tile count,
+// to nearest, within [1, ks_max] and [1, js_max]; so a launch has at most
+// max(4/3 slots, rounded tile count) items and at most ks_max (js_max) times
+// the rounded tile count, whichever is less (the host sizes grids by that).
+enum SliceKind { kRowSlices, kColSlices };
+
 struct Plan {
-  int n_tiles, JS, W, n_items;
+  int n_tiles, KS, KR, JS, W, n_items;
 };
 
-__device__ __forceinline__ Plan make_plan(const ApplyArgs& g, bool slices) {
+__device__ __forceinline__ Plan make_plan(const ApplyArgs& g, SliceKind kind) {
   Plan p;
   const int nt = g.meta[4];
   p.n_tiles = nt < 0 ? 0 : (nt > g.tile_cap ? g.tile_cap : nt);
   const int n8 = (p.n_tiles + 7) & ~7;
-  int js = 1;
-  if (slices && n8 > 0) js = max(1, min(g.js_max, (g.slots + n8 / 2) / n8));
+  int ks = 1, js = 1;
+  if (n8 > 0) {
+    const int fit = (g.slots + n8 / 2) / n8;
+    ks = max(1, min(g.ks_max, fit));
+    js = max(1, min(g.js_max, fit));
+  }
+  p.KR = ((g.h_in + ks - 1) / ks + 63) & ~63;
+  p.KS = (g.h_in + p.KR - 1) / p.KR;
   p.W = ((g.h_out + js - 1) / js + 15) & ~15;
   p.JS = (g.h_out + p.W - 1) / p.W;
-  p.n_items = n8 * p.JS;
+  p.n_items = n8 * (kind == kRowSlices ? p.KS : p.JS);
   return p;
 }
 
@@ -545,22 +586,30 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
   t.Bi = g.B + bo;
   t.k0 = 0;
   t.k1 = g.h_in;
+  t.j0 = 0;
+  t.j1 = g.h_out;
   return true;
 }
 
 // Item i of plan p: items are numbered in groups of eight tiles, slice-major
-// inside a group, so that item i belongs to tile 8 * (i / (8 JS)) + i % 8;
-// with a grid that is a multiple of 8, all slices of a tile then run on work
-// groups with the same blockIdx.x mod 8, that is, on one XCD.
-__device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, int i, Tile& t,
-                                          int& my_tok) {
-  const int per = 8 * p.JS;
+// inside a group, so that item i is slice (i mod 8S) / 8 of tile
+// 8 (i / 8S) + i mod 8, S the slice count; a tile's slices are dispatched
+// together, and land on one XCD (work group b runs on XCD b mod 8).
+__device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, SliceKind kind,
+                                          int i, Tile& t, int& my_tok, int& slice) {
+  const int per = 8 * (kind == kRowSlices ? p.KS : p.JS);
   const int q = i / per, rem = i - q * per;
   const int u = 8 * q + (rem & 7);
   if (u >= p.n_tiles) return false;
   if (!load_tile(g, u, t, my_tok)) return false;
-  t.j0 = (rem >> 3) * p.W;
-  t.j1 = min(g.h_out, t.j0 + p.W);
+  slice = rem >> 3;
+  if (kind == kRowSlices) {
+    t.k0 = slice * p.KR;
+    t.k1 = min(g.h_in, t.k0 + p.KR);
+  } else {
+    t.j0 = slice * p.W;
+    t.j1 = min(g.h_out, t.j0 + p.W);
+  }
   return true;
 }
 
@@ -608,10 +657,14 @@ __device__ __forceinline__ Smem carve(void* base, int max_rank) {
 constexpr int ilog2(int v) { return v <= 1 ? 0 : 1 + ilog2(v / 2); }
 
 // ---------------------------------------------------------------------------
-// tiles of up to kVT tokens: vector ALU
+// short tiles: vector ALU
 // ---------------------------------------------------------------------------
 
-constexpr int kVT = 4;               // longest tile on the vector path
+// Longest tile on the vector path: two tokens at ranks up to 16, four at
+// ranks of 32 and more.  At the larger ranks a matrix-path stage of A_i fills
+// the wavefront's LDS ring in two or three stages, too shallow to stream
+// A_i as fast as the vector path's register prefetch does.
+__device__ __forceinline__ int vector_tokens(int r) { return r >= 32 ? 4 : 2; }
 
 // A_i and B_i chunks per thread requested up front for TG tokens: wider
 // token groups hold more accumulators and x words, so they prefetch less.
@@ -1033,7 +1086,7 @@ __device__ __forceinline__ u32x4_t lds_b128(uint32_t a) {
   return v;
 }
 
-// Shrink of a tile of more than kVT tokens on the matrix cores, for rank R:
+// Shrink of a longer tile on the matrix cores, for rank R:
 // MT M tiles of 16 tokens, NTN N tiles of 16 columns (R = 8 uses the first
 // half of one; its other columns are read past the row end and never
 // stored).  Wavefront w takes the K steps (32 rows of h_in) w, w + kW, ...,
@@ -1365,7 +1418,7 @@ __device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, con
 __device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
                                               const Smem& sm, bool do_shrink,
                                               bool do_expand) {
-  if (t.L > kVT) mfma_tile(g, t, sm, do_shrink, do_expand);
+  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, do_shrink, do_expand);
   else valu_tile(g, t, sm, do_shrink, do_expand);
 }
 
@@ -1382,48 +1435,83 @@ __device__ __forceinline__ Smem tile_prologue(const ApplyArgs& g, int my_tok, vo
 // kernels
 // ---------------------------------------------------------------------------
 
-// plora_shrink: one item per tile; v of each valid token to g.v.
-__global__ __launch_bounds__(kNT, kWGPerCU) void shrink_kernel(ApplyArgs g) {
+// Shrink launch (plora_apply, plora_shrink): item (tile, h_in slice) writes
+// the slice's partial v of the tile's rows to the workspace.
+__global__ __launch_bounds__(kNT, kWGPerCU) void shrink_part_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
-  const Plan p = make_plan(g, false);
+  const Plan p = make_plan(g, kRowSlices);
   Tile t;
-  int my_tok;
-  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
+  int my_tok, ks;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, kRowSlices, blockIdx.x, t, my_tok, ks))
+    return;
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
   tile_dispatch(g, t, sm, true, false);
+  float* dst = g.vpart + ((int64_t)ks * g.T + t.p0) * g.max_rank;
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
-    const int tk = sm.tok[l];
-    if (tk >= 0) g.v[(int64_t)tk * g.ldv + c] = sm.vs[c * kTT + l];
+    dst[l * g.max_rank + c] = sm.vs[c * kTT + l];
   }
 }
 
-// plora_expand: the fused apply's items, with v read from g.v.
+// plora_apply as one launch: the tile's shrink over all of h_in, then the
+// expand of the item's column slice.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  const Plan p = make_plan(g, kColSlices);
+  Tile t;
+  int my_tok, js;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, kColSlices, blockIdx.x, t, my_tok, js))
+    return;
+  const Smem sm = tile_prologue(g, my_tok, apply_lds);
+  tile_dispatch(g, t, sm, true, true);
+}
+
+// v of tile row l, column c: the sum of the KS partials in slice order.
+__device__ __forceinline__ float sum_parts(const ApplyArgs& g, const Plan& p, const Tile& t,
+                                           int l, int c) {
+  const float* src = g.vpart + (int64_t)(t.p0 + l) * g.max_rank + c;
+  const int64_t step = (int64_t)g.T * g.max_rank;
+  float v = src[0];
+  for (int ks = 1; ks < p.KS; ++ks) v += src[ks * step];
+  return v;
+}
+
+// Expand launch: item (tile, y column slice) takes the tile's v from the
+// workspace partials (plora_apply) or from g.v (plora_expand) and expands it.
+template <bool FROM_PARTS>
 __global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
-  const Plan p = make_plan(g, true);
+  const Plan p = make_plan(g, kColSlices);
   Tile t;
-  int my_tok;
-  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
+  int my_tok, js;
+  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, kColSlices, blockIdx.x, t, my_tok, js))
+    return;
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
   for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
-    const int tk = sm.tok[l];
-    sm.vs[c * kTT + l] = tk >= 0 ? g.v[(int64_t)tk * g.ldv + c] : 0.f;
+    if (FROM_PARTS) {
+      sm.vs[c * kTT + l] = sum_parts(g, p, t, l, c);
+    } else {
+      const int tk = sm.tok[l];
+      sm.vs[c * kTT + l] = tk >= 0 ? g.v[(int64_t)tk * g.ldv + c] : 0.f;
+    }
   }
   lds_sync();
   tile_dispatch(g, t, sm, false, true);
 }
 
-// plora_apply: the tile's shrink, then the expand of the item's slice.
-__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
-  extern __shared__ __align__(16) unsigned char apply_lds[];
-  const Plan p = make_plan(g, true);
+// plora_shrink's second launch: v of each valid token of tile blockIdx.x,
+// summed from the partials as the expand launch sums them.
+__global__ __launch_bounds__(kNT) void gather_v_kernel(ApplyArgs g) {
+  const Plan p = make_plan(g, kRowSlices);
   Tile t;
   int my_tok;
-  if ((int)blockIdx.x >= p.n_items || !item_tile(g, p, blockIdx.x, t, my_tok)) return;
-  const Smem sm = tile_prologue(g, my_tok, apply_lds);
-  tile_dispatch(g, t, sm, true, true);
+  if ((int)blockIdx.x >= p.n_tiles || !load_tile(g, blockIdx.x, t, my_tok)) return;
+  for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
+    const int l = o / t.r, c = o - l * t.r;
+    const int tk = g.perm[t.p0 + l];
+    if (tk >= 0 && tk < g.T) g.v[(int64_t)tk * g.ldv + c] = sum_parts(g, p, t, l, c);
+  }
 }
 
 __global__ void zero_kernel(uint4* p, size_t n16) {
@@ -1469,12 +1557,25 @@ int cu_count() {
 int slots_for_device() { return std::max(8, cu_count() * kWGPerCU); }
 
 // One work group per item: the most items make_plan can produce for any tile
-// count up to tile_cap (see there).
-unsigned grid_for(const ApplyArgs& g, bool slices) {
+// count up to tile_cap with at most s_max slices per tile (see there).
+unsigned grid_for(const ApplyArgs& g, int s_max) {
   const int64_t cap8 = (g.tile_cap + 7) & ~7;
-  if (!slices || g.js_max == 1) return (unsigned)std::max<int64_t>(8, cap8);
+  if (s_max <= 1) return (unsigned)std::max<int64_t>(8, cap8);
   const int64_t spread = ((int64_t)g.slots * 4 / 3 + 8 + 7) & ~7;
-  return (unsigned)std::max<int64_t>(8, std::min(cap8 * g.js_max, std::max(cap8, spread)));
+  return (unsigned)std::max<int64_t>(8, std::min(cap8 * s_max, std::max(cap8, spread)));
+}
+
+// Most h_in slices per tile: slices of at least 512 rows, at most 8.
+int ks_max_for(int h_in) { return std::max(1, std::min(8, h_in / 512)); }
+
+// plora_apply runs as one launch for batches of up to kFusedTokens tokens;
+// plora_shrink then takes one h_in slice, so that its v carries the very
+// bits the fused launch computes.
+bool fused_for(int32_t T) { return T <= kFusedTokens; }
+
+size_t workspace_bytes(int32_t T, const plora_adapters* ad) {
+  if (!ad || T <= 0 || ad->h_in <= 0 || ad->max_rank <= 0) return 0;
+  return (size_t)ks_max_for(ad->h_in) * T * ad->max_rank * sizeof(float);
 }
 
 plora_status check_adapters_host(const plora_adapters* ad) {
@@ -1522,8 +1623,7 @@ plora_status launch_status() {
 }
 
 plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* ws,
-                     size_t ws_bytes, ApplyArgs& g) {
-  (void)ws; (void)ws_bytes;  // the tile kernels need no workspace
+                     size_t ws_bytes, ApplyArgs& g, bool needs_ws) {
   plora_status st = check_adapters_host(ad);
   if (st != PLORA_OK) return st;
   st = check_segments_host(seg, ad->n_adapters);
@@ -1536,8 +1636,16 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   g.meta = seg->meta;
   g.T = seg->T; g.N = ad->n_adapters; g.h_in = ad->h_in; g.h_out = ad->h_out;
   g.max_rank = ad->max_rank; g.tile_cap = seg->tile_cap;
+  g.ks_max = fused_for(seg->T) ? 1 : ks_max_for(ad->h_in);
   g.js_max = std::max(1, ad->h_out / kMinSlice);
   g.slots = slots_for_device();
+  if (needs_ws && seg->T > 0) {
+    const size_t need = workspace_bytes(seg->T, ad);
+    if (!ws) return PLORA_ERR_INVALID_ARG;
+    if (!aligned16(ws)) return PLORA_ERR_UNSUPPORTED;
+    if (ws_bytes < need) return PLORA_ERR_WORKSPACE_TOO_SMALL;
+    g.vpart = reinterpret_cast<float*>(ws);
+  }
   return PLORA_OK;
 }
 
@@ -1549,14 +1657,15 @@ void allow_lds(const void* kernel, std::atomic<bool>& done) {
   done.store(true);
 }
 
-std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false};
+std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false},
+    g_lds_parts{false};
 
 template <class K>
 plora_status launch_items(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
-                          bool slices, hipStream_t stream) {
+                          int s_max, hipStream_t stream) {
   const size_t lds = smem_bytes(g.h_in, g.max_rank);
   if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(kernel), lds_done);
-  const unsigned grid = grid_for(g, slices);
+  const unsigned grid = grid_for(g, s_max);
   clear_stale_error();
   hipLaunchKernelGGL(kernel, dim3(grid), dim3(kNT), lds, stream, g);
   return launch_status();
@@ -1577,8 +1686,7 @@ int32_t plora_tile_capacity(int32_t T, int32_t n_adapters) {
 }
 
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad) {
-  (void)T; (void)ad;
-  return 0;
+  return workspace_bytes(T, ad);
 }
 
 plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -1630,42 +1738,49 @@ plora_status plora_shrink(const uint16_t* x, int64_t ldx, const plora_adapters* 
                           const plora_segments* seg, float* v, int64_t ldv, void* ws,
                           size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g, true);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!x || !v) return PLORA_ERR_INVALID_ARG;
   if (ldx < ad->h_in || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldv & 3) || !aligned16(x) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.v = v; g.ldv = ldv;
-  return launch_items(shrink_kernel, g_lds_shrink, g, false, stream);
+  st = launch_items(shrink_part_kernel, g_lds_shrink, g, g.ks_max, stream);
+  if (st != PLORA_OK) return st;
+  clear_stale_error();
+  hipLaunchKernelGGL(gather_v_kernel, dim3((unsigned)g.tile_cap), dim3(kNT), 0, stream, g);
+  return launch_status();
 }
 
 plora_status plora_expand(const float* v, int64_t ldv, const plora_adapters* ad,
                           const plora_segments* seg, uint16_t* y, int64_t ldy, void* ws,
                           size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g, false);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!v || !y) return PLORA_ERR_INVALID_ARG;
   if (ldy < ad->h_out || ldv < ad->max_rank) return PLORA_ERR_INVALID_ARG;
   if ((ldy & 7) || (ldv & 3) || !aligned16(y) || !aligned16(v)) return PLORA_ERR_UNSUPPORTED;
   g.v = const_cast<float*>(v); g.ldv = ldv; g.y = y; g.ldy = ldy;
-  return launch_items(expand_kernel, g_lds_expand, g, true, stream);
+  return launch_items(expand_kernel<false>, g_lds_expand, g, g.js_max, stream);
 }
 
 plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* ad,
                          const plora_segments* seg, uint16_t* y, int64_t ldy, void* ws,
                          size_t ws_bytes, hipStream_t stream) {
   ApplyArgs g;
-  plora_status st = prepare(ad, seg, ws, ws_bytes, g);
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g, true);
   if (st != PLORA_OK) return st;
   if (seg->T == 0) return PLORA_OK;
   if (!x || !y) return PLORA_ERR_INVALID_ARG;
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
-  return launch_items(apply_kernel, g_lds_apply, g, true, stream);
+  if (fused_for(seg->T)) return launch_items(apply_kernel, g_lds_apply, g, g.js_max, stream);
+  st = launch_items(shrink_part_kernel, g_lds_shrink, g, g.ks_max, stream);
+  if (st != PLORA_OK) return st;
+  return launch_items(expand_kernel<true>, g_lds_parts, g, g.js_max, stream);
 }
 
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,

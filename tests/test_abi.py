@@ -78,10 +78,24 @@ def _apply_status(ad=None, seg=None, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
                              ws_bytes, None)
 
 
-def test_no_workspace_needed():
+def test_workspace_size_and_checks():
+    # partial sums of v over min(8, h_in / 512) slices of h_in, fp32
+    for h_in, k in [(256, 1), (1024, 2), (4096, 8), (32768, 8)]:
+        ad = _ad(h_in=h_in, max_rank=16)
+        assert P.plora_workspace_bytes(100, ad) == k * 100 * 16 * 4
     ad = _ad()
-    assert P.plora_workspace_bytes(8, ad) == 0
+    assert P.plora_workspace_bytes(0, ad) == 0
     assert P.lib.plora_workspace_init(None, 0, None) == P.PLORA_OK
+    need = P.plora_workspace_bytes(8, ad)
+    assert need > 0
+    assert _apply_status(ws_bytes=need - 16) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
+    assert _apply_status(ws=None) == P.PLORA_ERR_INVALID_ARG
+    assert _apply_status(ws=FAKE + 8) == P.PLORA_ERR_UNSUPPORTED
+    # plora_expand takes no workspace: its checks pass with none (T = 0 so
+    # nothing is launched on the fake pointers)
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    assert P.lib.plora_expand(FAKE, 8, ctypes.byref(ad), ctypes.byref(empty), FAKE, 256,
+                              None, 0, None) == P.PLORA_OK
 
 
 def test_large_model_dimensions_pass_host_checks():
