@@ -22,9 +22,10 @@
  *   plora_segment  group tokens by adapter id (stable counting sort)
  *   plora_shrink   v[t, :] = x[t, :] A_i            (E4's m = xA, fp32)
  *   plora_expand   y[t, :] += s_i v[t, :] B_i        (E4's y = mB)
- *   plora_apply    both: one launch for batches of up to 1024 tokens (v
- *                  stays on chip), two above (per-slice partial sums of v,
- *                  fp32, pass through the workspace)
+ *   plora_apply    both: one launch for batches of up to 1024 tokens, two
+ *                  above (per-slice partial sums of v, fp32, pass through the
+ *                  workspace; within the one launch too when a tile is
+ *                  split among several work groups)
  *
  * Data types and layouts (all row-major, element strides):
  *   x       bf16 [T, ldx], first h_in columns used
@@ -36,7 +37,9 @@
  * Arithmetic: bf16 x bf16 products are exact in fp32; all sums are fp32;
  * v is never rounded below fp32; y is rounded once, to nearest even.
  * Reduction orders are fixed, so every call is bitwise deterministic, and
- * plora_apply equals plora_shrink followed by plora_expand bit for bit.
+ * plora_apply equals plora_shrink followed by plora_expand bit for bit
+ * (one exception, under plora_apply: a work group whose partners were not
+ * scheduled in time).
  *
  * Memory and ownership: every pointer below is a DEVICE pointer unless the
  * text says "host"; the caller allocates and owns every buffer, including
@@ -168,16 +171,25 @@ typedef struct {
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 
 /* Host.  Bytes of device workspace plora_apply and plora_shrink need for a
- * batch of up to T tokens over this adapter stack: the partial sums of v over
- * up to 8 slices of h_in, fp32, K * T * max_rank * 4 bytes with
- * K = min(8, max(1, h_in / 512)); 0 for T <= 0.  The workspace needs no
- * initialisation (every partial is written before it is read) and holds
- * nothing between calls; calls that share one must not overlap in time.
- * plora_segment and plora_expand take none (ws may be NULL). */
+ * batch of up to T tokens over this adapter stack; 0 for T <= 0.  Three
+ * sections, each starting on a 256-byte boundary:
+ *   1. the epochs of the one-launch apply's tile slots: 336 64-bit words;
+ *   2. its exchange regions: 8 * 32 * 128 64-bit words for each of
+ *      P = min(336, max(8, cap8)) tile slots, cap8 being
+ *      plora_tile_capacity(T, N) rounded up to a multiple of 8;
+ *   3. the partial sums of v over up to 8 slices of h_in, fp32,
+ *      K * T * max_rank * 4 bytes with K = min(8, max(1, h_in / 512)).
+ * Sections 1 and 2 keep their offsets whatever T, the ranks or the slice
+ * count, so one workspace serves calls of any batch size up to T and any
+ * adapter stack it is large enough for.  Zero it once with
+ * plora_workspace_init before its first use; afterwards it carries the
+ * epochs from call to call and must not be written by the caller.  Calls
+ * that share one must not overlap in time.  plora_segment and plora_expand
+ * take none (ws may be NULL). */
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad);
 
-/* Zero a workspace (enqueued on stream; a no-op for ws_bytes == 0).  Not
- * required by any call; for callers that want defined contents. */
+/* Zero a workspace (enqueued on stream; a no-op for ws_bytes == 0), as
+ * plora_apply requires once before a workspace's first use. */
 plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
@@ -217,8 +229,15 @@ plora_status plora_expand(const float* v, int64_t ldv,
  * (strategy E1: both matrices resident in GPU memory, section V-A).  For
  * T <= 1024 one launch; above, two launches with v's partial sums passed
  * through ws.  ws must hold plora_workspace_bytes(T) bytes, 16-byte aligned,
- * in both cases.  Bit for bit the same as plora_shrink followed by
- * plora_expand.  x and y must not overlap.
+ * zeroed once by plora_workspace_init before its first use, in both cases.
+ * When a batch has few tiles (the decode case), each tile is reduced by up
+ * to 8 work groups of the launch, which trade their partial sums of v
+ * through ws; a work group never waits for another without bound: if a
+ * partner does not publish within a bounded number of polls (it was not
+ * scheduled), the work group computes v by itself, which is correct to fp32
+ * accuracy but summed in another order.  Apart from that case the result is
+ * bit for bit the same as plora_shrink followed by plora_expand, and
+ * bitwise deterministic.  x and y must not overlap.
  */
 plora_status plora_apply(const uint16_t* x, int64_t ldx,
                          const plora_adapters* ad, const plora_segments* seg,
@@ -241,6 +260,13 @@ const char* plora_status_string(plora_status status);
 /* Test hook: the hipError_t of the most recent launch that returned
  * PLORA_ERR_HIP in this process, 0 if none did. */
 int32_t plora_debug_last_hip_error(void);
+
+/* Test hook: how many times a one-launch plora_apply work item re-reads a
+ * partner's partial v before computing v by itself (see plora_apply), for
+ * calls made after this one in this process; a negative value restores the
+ * default (20000).  0 makes every item whose partners have not yet
+ * published take the self-computed path, which tests can then check. */
+void plora_debug_set_exchange_polls(int32_t polls);
 
 #ifdef __cplusplus
 }

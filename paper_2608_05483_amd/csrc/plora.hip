@@ -11,8 +11,10 @@
 //   plora_expand   PLORA_TILE_TOKENS tokens of one adapter, section VI-B's
 //   plora_apply    per-adapter batch B_i split into tiles) and one slice of
 //                  h_in or of the y columns; plora_apply is one launch for
-//                  batches of up to kFusedTokens tokens and two above;
-//                  details above the apply kernels below.
+//                  batches of up to kFusedTokens tokens (with the tile's
+//                  slices exchanging partial v through the workspace when
+//                  the batch has few tiles) and two above; details above the
+//                  apply kernels below.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -421,27 +423,32 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
 // ---------------------------------------------------------------------------
 //
 // Work items.  An item is one tile and one slice of h_in (KS slices of KR
-// rows) or of the y columns (JS slices of W columns).  KS and JS are chosen
-// on the device from the tile count that plora_segment wrote, so that each
-// launch has about one item per resident work group (two per compute unit)
-// and a batch of a few dozen tiles still spreads over the whole chip; the
-// host sizes each grid to the most items any tile count can produce, and
-// surplus work groups return after one load.  Nothing passes between work
-// groups inside a launch: that would need agent-scope release and acquire,
-// an L2 write-back across XCDs on MI355X.  plora_apply takes one of two
-// forms, by batch size:
+// rows) or of the y columns (JS slices of W columns), so that each launch
+// has about one item per resident work group (two per compute unit) and a
+// batch of a few dozen tiles still spreads over the whole chip.  plora_apply
+// takes one of three forms, by batch size:
 //
-//   one launch (up to kFusedTokens tokens, decode batches): item (tile,
-//   column slice) computes the tile's v over all of h_in, then expands it
-//   with its slice of B_i.  A_i is read by every column slice of its tile;
-//   the slices of a tile are numbered onto one XCD, so the first read brings
-//   A_i into that XCD's L2 and the others hit it.  One launch boundary fewer
-//   is worth more than the repeated L2 reads when the batch is small.
+//   one launch, S > 1 slices per tile (batches whose tile capacity is at
+//   most 2/3 of the resident work groups: decode batches).  S is chosen on
+//   the host from the tile capacity; item (tile, s) reduces h_in slice s,
+//   trades partial v with the tile's other items through the workspace (see
+//   the exchange below) and expands y column slice s.  Each item reads 1/S
+//   of A_i and of B_i.
+//
+//   one launch, one h_in slice (up to kFusedTokens tokens otherwise): item
+//   (tile, column slice), JS chosen on the device from the tile count that
+//   plora_segment wrote, computes the tile's v over all of h_in, then
+//   expands it with its slice of B_i.  A_i is read by every column slice of
+//   its tile; the slices of a tile are numbered onto one XCD, so the first
+//   read brings A_i into that XCD's L2 and the others hit it.
 //
 //   two launches (larger batches, where x dominates): item (tile, h_in
 //   slice) writes its partial v to the workspace; item (tile, column slice)
 //   sums the tile's KS partials in slice order and expands.  Every byte of
 //   A_i, B_i and x is then read by one work group only.
+//
+// Grids are sized on the host for the most items any tile count up to the
+// capacity can produce; surplus work groups return after one load.
 //
 // Two code paths, chosen per tile:
 //
@@ -515,9 +522,13 @@ struct ApplyArgs {
   const int32_t* meta;
   int32_t T, N, h_in, h_out, max_rank, tile_cap;
   float* vpart;         // workspace: partial v [ks_max][T][max_rank]
+  uint64_t* xw;         // workspace: exchange words [S][cap8][kTT][max_rank] (one launch)
+  uint64_t* xep;        // workspace: exchange epoch per tile slot [cap8]
   int32_t ks_max;      // most h_in slices per tile
   int32_t js_max;      // most y column slices per tile
   int32_t slots;       // resident work groups the device holds (item target)
+  int32_t fixed_slices; // > 0: every tile takes exactly this many h_in and y column slices
+  int32_t polls;        // polls of a partner's exchange word before computing v alone
 };
 
 struct Tile {
@@ -550,7 +561,9 @@ __device__ __forceinline__ Plan make_plan(const ApplyArgs& g, SliceKind kind) {
   p.n_tiles = nt < 0 ? 0 : (nt > g.tile_cap ? g.tile_cap : nt);
   const int n8 = (p.n_tiles + 7) & ~7;
   int ks = 1, js = 1;
-  if (n8 > 0) {
+  if (g.fixed_slices > 0) {
+    ks = js = g.fixed_slices;
+  } else if (n8 > 0) {
     const int fit = (g.slots + n8 / 2) / n8;
     ks = max(1, min(g.ks_max, fit));
     js = max(1, min(g.js_max, fit));
@@ -1004,12 +1017,108 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
   }
 }
 
-template <int TG>
+// ---------------------------------------------------------------------------
+// one-launch apply: exchange of a tile's partial v between its slices
+// ---------------------------------------------------------------------------
+//
+// In the one-launch form every tile is split into S items; item s reduces
+// rows [s KR, (s+1) KR) of h_in (its partial v) and expands y columns
+// [s W, (s+1) W).  Each item needs the full v, the sum of all S partials.
+// Items publish their partial as 64-bit words {fp32 bits, tag} in a region
+// of the workspace private to the tile slot (slot = tile index), and each
+// item polls its partners' words until every one carries this call's tag.
+// Tags come from a 64-bit epoch per tile slot, read when the item starts
+// and raised (atomic max) to epoch + 1 when it ends: every item of a call
+// reads the epoch before any partner can raise it (a partner raises it only
+// after it has seen every item's words, or after giving up), so the call's
+// tag is new to the slot's region, and stale words from earlier calls, other
+// batch sizes or other ranks never match (the tag is the epoch's low 32
+// bits: a word would have to lie unused for 2^32 calls of its slot).  The
+// state is on the device, so the scheme holds under graph replay too.
+// Polling is bounded: if a partner's word has not come after kSpinLimit
+// polls (the partner was never scheduled, say because other work holds the
+// compute units), the item computes v over all of h_in by itself (plain_v):
+// correct to fp32 accuracy, but summed in another order, so such a call's
+// bits can differ from the usual result.  No item ever waits without bound.
+// The split into slices serves small batches, where a tile's reduction
+// spread over S work groups (each reading 1/S of A_i and of B_i) beats one
+// work group streaming all of A_i; the exchange costs about one memory
+// round trip, which the expand's first loads of B_i and y overlap.
+
+constexpr int kMaxSlices = 8;            // most slices per tile in the one-launch form
+constexpr int kXSlots = 336;             // tile slots with an exchange region
+constexpr int kSlotTarget = 512;         // resident work groups the plans aim at (256 CUs x 2)
+constexpr int kSpinLimit = 20000;        // polls of a partner's word before computing v alone
+constexpr int64_t kSlotWords = (int64_t)kMaxSlices * kTT * PLORA_MAX_RANK;   // words per slot
+
+struct Xchg {
+  int s, S, kr;          // this item's slice, the tile's slice count, rows of h_in per slice
+  uint32_t tag;          // this call's tag for the tile slot
+  uint64_t* words;       // the slot's region: [kTT * PLORA_MAX_RANK][kMaxSlices]
+  int polls;             // polls before giving up on a partner
+};
+
+__device__ __forceinline__ uint64_t xload(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Publish this item's partial v (sm.vs) and replace sm.vs by the sum of all
+// S partials, in slice order (the order plora_shrink and the two-launch form
+// sum them in).  Entry o = l r + c of the tile keeps its kMaxSlices words
+// side by side, so one address serves all of them.  A word carrying this
+// call's tag never changes again during the call, so a poll simply reloads
+// every word of the entry.  Returns false, for the whole work group, if some
+// partner's word did not arrive in time; sm.vs is then undefined.
+__device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const Xchg& xc) {
+  const int n = t.L * t.r;
+  const uint64_t tagw = (uint64_t)xc.tag << 32;
+  for (int o = threadIdx.x; o < n; o += kNT) {
+    const int l = o / t.r, c = o - l * t.r;
+    __hip_atomic_store(xc.words + o * kMaxSlices + xc.s,
+                       tagw | __float_as_uint(sm.vs[c * kTT + l]), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  }
+  bool late = false;
+  for (int o = threadIdx.x; o < n; o += kNT) {
+    const uint64_t* e = xc.words + o * kMaxSlices;
+    uint64_t w[kMaxSlices];
+    bool ready = false;
+    for (int it = 0; !ready && it <= xc.polls; ++it) {
+      if (it > 0) __builtin_amdgcn_s_sleep(2);
+#pragma unroll
+      for (int q = 0; q < kMaxSlices; ++q) w[q] = xload(e + q);
+      ready = true;
+#pragma unroll
+      for (int q = 0; q < kMaxSlices; ++q)
+        ready &= q >= xc.S || (uint32_t)(w[q] >> 32) == xc.tag;
+    }
+    late |= !ready;
+    float v = __uint_as_float((uint32_t)w[0]);
+#pragma unroll
+    for (int q = 1; q < kMaxSlices; ++q)
+      if (q < xc.S) v += __uint_as_float((uint32_t)w[q]);
+    const int l = o / t.r, c = o - l * t.r;
+    sm.vs[c * kTT + l] = v;
+  }
+  return __syncthreads_or(late) == 0;
+}
+
+// An expand-only call with a hook (the one-launch form's exchange of v)
+// requests its first chunks of B_i and its y words, then runs the hook,
+// which leaves the final v in sm.vs, then expands: the loads travel while
+// the hook waits.
+struct NoHook {
+  __device__ void operator()() const {}
+};
+
+template <int TG, class H>
 __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                             bool do_shrink, bool do_expand) {
+                                             bool do_shrink, bool do_expand, bool hooked,
+                                             H&& hook) {
   uint4 bpre[bp_depth<TG>()], ypre[TG];
 #pragma unroll
   for (int i = 0; i < TG; ++i) ypre[i] = make_uint4(0, 0, 0, 0);
+  bool have_y = do_shrink;
   if (do_shrink) {
     switch (t.r >> 3) {
       case 1: shrink_valu<1, TG>(g, t, sm, bpre, ypre, do_expand); break;
@@ -1020,15 +1129,21 @@ __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, 
     }
   } else {
     prefetch_b<bp_depth<TG>()>(g, t, bpre);
+    if (hooked) {
+      prefetch_y<TG>(g, t, sm.tok, ypre);
+      hook();
+      have_y = true;
+    }
   }
-  if (do_expand) expand_valu<TG>(g, t, sm, bpre, ypre, do_shrink);
+  if (do_expand) expand_valu<TG>(g, t, sm, bpre, ypre, have_y);
 }
 
+template <class H>
 __device__ __forceinline__ void valu_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                          bool do_shrink, bool do_expand) {
-  if (t.L == 1) valu_tile_tg<1>(g, t, sm, do_shrink, do_expand);
-  else if (t.L == 2) valu_tile_tg<2>(g, t, sm, do_shrink, do_expand);
-  else valu_tile_tg<4>(g, t, sm, do_shrink, do_expand);
+                                          bool do_shrink, bool do_expand, bool hooked, H&& hook) {
+  if (t.L == 1) valu_tile_tg<1>(g, t, sm, do_shrink, do_expand, hooked, hook);
+  else if (t.L == 2) valu_tile_tg<2>(g, t, sm, do_shrink, do_expand, hooked, hook);
+  else valu_tile_tg<4>(g, t, sm, do_shrink, do_expand, hooked, hook);
 }
 
 // ---------------------------------------------------------------------------
@@ -1271,8 +1386,9 @@ __device__ __forceinline__ void split_v(const Tile& t, const Smem& sm, int RK) {
 
 // Expand of a multi-token tile with MT token tiles of 16: D^T[j][token] =
 // sum_c B_i[c][j] (vhi + vlo)[token][c], then y = bf16(y + s D).
-template <int MT>
-__device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+template <int MT, class H>
+__device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                            H&& hook) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4;
   const int r = t.r;
   const int RK = rk_max(g.max_rank);
@@ -1323,15 +1439,9 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       *reinterpret_cast<uint4*>(Bs + r * S + q * 8) = make_uint4(0, 0, 0, 0);
   };
 
-  load_b(t.j0);
-  for (int ch = 0; ch < nchunks; ++ch) {
-    const int j0 = t.j0 + ch * JC;
-    const int cols = min(JC, t.j1 - j0);
-    const int S = (cols + 15) / 16 * 16;
-    const int njt = S / 16;
-    store_b(j0);
-    lds_sync();
-    // y words of this wave's j tiles, then the next chunk of B_i
+  // y words of this wave's j tiles of the chunk starting at column j0
+  auto load_y = [&](int j0) {
+    const int njt = (min(JC, t.j1 - j0) + 15) / 16;
 #pragma unroll
     for (int i = 0; i < JT; ++i) {
       const int jt = w + i * kW;
@@ -1341,6 +1451,21 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       for (int nt = 0; nt < MT; ++nt)
         yv[i][nt] = ldg8c(g.y + (int64_t)toks[nt] * g.ldy + j, jok && toks[nt] >= 0);
     }
+  };
+
+  // the first chunk's B_i and y are requested before the hook runs
+  load_b(t.j0);
+  load_y(t.j0);
+  hook();
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int j0 = t.j0 + ch * JC;
+    const int cols = min(JC, t.j1 - j0);
+    const int S = (cols + 15) / 16 * 16;
+    const int njt = S / 16;
+    store_b(j0);
+    lds_sync();
+    // y words of this chunk (the first came before), then the next chunk of B_i
+    if (ch > 0) load_y(j0);
     if (ch + 1 < nchunks) load_b(j0 + JC);
 #pragma unroll
     for (int i = 0; i < JT; ++i) {
@@ -1380,46 +1505,67 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
   }
 }
 
+__device__ __forceinline__ void shrink_mfma_r(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  if (t.L > 16) {
+    switch (t.r) {
+      case 8: shrink_mfma<2, 8>(g, t, sm); break;
+      case 16: shrink_mfma<2, 16>(g, t, sm); break;
+      case 32: shrink_mfma<2, 32>(g, t, sm); break;
+      case 64: shrink_mfma<2, 64>(g, t, sm); break;
+      default: shrink_mfma<2, 128>(g, t, sm); break;
+    }
+  } else {
+    switch (t.r) {
+      case 8: shrink_mfma<1, 8>(g, t, sm); break;
+      case 16: shrink_mfma<1, 16>(g, t, sm); break;
+      case 32: shrink_mfma<1, 32>(g, t, sm); break;
+      case 64: shrink_mfma<1, 64>(g, t, sm); break;
+      default: shrink_mfma<1, 128>(g, t, sm); break;
+    }
+  }
+}
+
+template <class H>
 __device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                          bool do_shrink, bool do_expand) {
+                                          bool do_shrink, bool do_expand, bool hooked, H&& hook) {
   const int RK = rk_max(g.max_rank);
   // v's bf16 split is read for every token row < 16 * MT and column < K extent
   for (int o = threadIdx.x; o < 2 * kTT * RK; o += kNT) sm.vhl[o] = 0;
   lds_sync();
   const bool two = t.L > 16;
   if (do_shrink) {
-    if (two) {
-      switch (t.r) {
-        case 8: shrink_mfma<2, 8>(g, t, sm); break;
-        case 16: shrink_mfma<2, 16>(g, t, sm); break;
-        case 32: shrink_mfma<2, 32>(g, t, sm); break;
-        case 64: shrink_mfma<2, 64>(g, t, sm); break;
-        default: shrink_mfma<2, 128>(g, t, sm); break;
-      }
-    } else {
-      switch (t.r) {
-        case 8: shrink_mfma<1, 8>(g, t, sm); break;
-        case 16: shrink_mfma<1, 16>(g, t, sm); break;
-        case 32: shrink_mfma<1, 32>(g, t, sm); break;
-        case 64: shrink_mfma<1, 64>(g, t, sm); break;
-        default: shrink_mfma<1, 128>(g, t, sm); break;
-      }
-    }
-  } else {
+    shrink_mfma_r(g, t, sm);
+  } else if (!hooked) {
     split_v(t, sm, RK);
     lds_sync();
   }
+  // with a hook, v is final only after it has run: split it then
+  auto after_b = [&] {
+    if (hooked) {
+      hook();
+      split_v(t, sm, RK);
+      lds_sync();
+    }
+  };
   if (do_expand) {
-    if (two) expand_mfma<2>(g, t, sm);
-    else expand_mfma<1>(g, t, sm);
+    if (two) expand_mfma<2>(g, t, sm, after_b);
+    else expand_mfma<1>(g, t, sm, after_b);
   }
 }
 
 __device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
                                               const Smem& sm, bool do_shrink,
                                               bool do_expand) {
-  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, do_shrink, do_expand);
-  else valu_tile(g, t, sm, do_shrink, do_expand);
+  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, do_shrink, do_expand, false, NoHook{});
+  else valu_tile(g, t, sm, do_shrink, do_expand, false, NoHook{});
+}
+
+// Expand only, with hook() run once the first loads of B_i are on their way.
+template <class H>
+__device__ __forceinline__ void expand_hooked(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                              H&& hook) {
+  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, false, true, true, hook);
+  else valu_tile(g, t, sm, false, true, true, hook);
 }
 
 // Common prologue: token indices to LDS, v zeroed.
@@ -1453,9 +1599,126 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void shrink_part_kernel(ApplyArgs g)
   }
 }
 
-// plora_apply as one launch: the tile's shrink over all of h_in, then the
-// expand of the item's column slice.
+// The values the one-launch item carries from phase to phase, parked in LDS
+// and read back (as wave-uniform values) before each phase, so that none of
+// them stays in registers across the inlined shrink and expand bodies.
+struct ItemStash {
+  int a, p0, L, r;
+  float s;
+  int u, slice;
+  int pad;
+  const uint16_t* Ai;
+  const uint16_t* Bi;
+  uint64_t ep;
+};
+
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ const uint16_t* uni(const uint16_t* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return reinterpret_cast<const uint16_t*>(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ Tile unstash(const ItemStash* st) {
+  Tile t;
+  t.a = uni(st->a);
+  t.p0 = uni(st->p0);
+  t.L = uni(st->L);
+  t.r = uni(st->r);
+  t.s = __int_as_float(uni(__float_as_int(st->s)));
+  t.Ai = uni(st->Ai);
+  t.Bi = uni(st->Bi);
+  return t;
+}
+
+// What the exchange yields, computed by this item alone when a partner's
+// words never came: v[l][c] = sum over all of h_in of x[tok_l][k] A_i[k][c],
+// one entry per thread at a time, k ascending, in fp32.  Kept plain and
+// small: it runs only if a partner work group was not scheduled within
+// kSpinLimit polls, and its sum order differs from the slices', so such a
+// call's v (and y) can differ from the usual result in the last bits.
+__device__ __forceinline__ void plain_v(const ApplyArgs& g, const Tile& t, const Smem& sm) {
+  const int n = t.L * t.r;
+  for (int o = threadIdx.x; o < n; o += kNT) {
+    const int l = o / t.r, c = o - l * t.r;
+    const int tk = sm.tok[l];
+    float v = 0.f;
+    if (tk >= 0) {
+      const uint16_t* xr = g.x + (int64_t)tk * g.ldx;
+      for (int k = 0; k < g.h_in; ++k)
+        v = fmaf(__uint_as_float((uint32_t)xr[k] << 16),
+                 __uint_as_float((uint32_t)t.Ai[(int64_t)k * t.r + c] << 16), v);
+    }
+    sm.vs[c * kTT + l] = v;
+  }
+  lds_sync();
+}
+
+// plora_apply as one launch, tiles in S > 1 slices: item blockIdx.x =
+// u S + s is slice s of tile u (S = g.fixed_slices, chosen on the host, so
+// the item needs no count from the device): the shrink of h_in rows
+// [s KR, (s+1) KR), the exchange of partial v with the tile's other items,
+// and the expand of y columns [s W, (s+1) W), whose first loads of B_i and
+// y are issued before the exchange waits.  A tile's items are neighbours
+// in the grid, so the work groups a tile waits on are dispatched with it.
+// If the exchange times out, plain_v computes v here.
 __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  {
+    const int S = g.fixed_slices;
+    const int u = (int)blockIdx.x / S, s = (int)blockIdx.x - u * S;
+    // the slot's epoch is requested together with the tile record (the host
+    // made sure u < kXSlots)
+    const uint64_t ep = u < g.tile_cap ? xload(g.xep + u) : 0;
+    Tile t;
+    int my_tok;
+    if (!load_tile(g, u, t, my_tok)) return;
+    if (threadIdx.x == 0) {
+      stash.a = t.a; stash.p0 = t.p0; stash.L = t.L; stash.r = t.r; stash.s = t.s;
+      stash.u = u; stash.slice = s; stash.Ai = t.Ai; stash.Bi = t.Bi; stash.ep = ep;
+    }
+    (void)tile_prologue(g, my_tok, apply_lds);     // ends with a barrier
+  }
+  const Smem sm = carve(apply_lds, g.max_rank);
+  const int S = g.fixed_slices;
+  const int KR = ((g.h_in + S - 1) / S + 63) & ~63;
+  {
+    Tile t = unstash(&stash);
+    t.k0 = uni(stash.slice) * KR;
+    t.k1 = min(g.h_in, t.k0 + KR);
+    t.j0 = 0;
+    t.j1 = g.h_out;
+    tile_dispatch(g, t, sm, true, false);
+  }
+  {
+    Tile t = unstash(&stash);
+    const int s = uni(stash.slice);
+    const int W = ((g.h_out + S - 1) / S + 15) & ~15;
+    t.k0 = 0;
+    t.k1 = g.h_in;
+    t.j0 = s * W;
+    t.j1 = min(g.h_out, t.j0 + W);
+    const Xchg xc{s, S, KR, (uint32_t)(stash.ep + 1), g.xw + (int64_t)uni(stash.u) * kSlotWords,
+                  g.polls};
+    expand_hooked(g, t, sm, [&] {
+      if (!exchange_v(t, sm, xc)) plain_v(g, t, sm);
+    });
+  }
+  if (threadIdx.x == 0)
+    __hip_atomic_fetch_max(g.xep + stash.u, stash.ep + 1, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// plora_apply as one launch, one slice per tile in h_in: item (tile,
+// column slice) computes the tile's v over all of h_in, then expands it
+// with its slice of B_i (column slices from the tile count, as make_plan
+// gives them).  A_i is read by every column slice of its tile; the slices
+// of a tile are numbered onto one XCD, so the first read brings A_i into
+// that XCD's L2 and the others hit it.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_cols_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   const Plan p = make_plan(g, kColSlices);
   Tile t;
@@ -1560,6 +1823,7 @@ int slots_for_device() { return std::max(8, cu_count() * kWGPerCU); }
 // count up to tile_cap with at most s_max slices per tile (see there).
 unsigned grid_for(const ApplyArgs& g, int s_max) {
   const int64_t cap8 = (g.tile_cap + 7) & ~7;
+  if (g.fixed_slices > 0) return (unsigned)std::max<int64_t>(8, cap8 * g.fixed_slices);
   if (s_max <= 1) return (unsigned)std::max<int64_t>(8, cap8);
   const int64_t spread = ((int64_t)g.slots * 4 / 3 + 8 + 7) & ~7;
   return (unsigned)std::max<int64_t>(8, std::min(cap8 * s_max, std::max(cap8, spread)));
@@ -1568,15 +1832,51 @@ unsigned grid_for(const ApplyArgs& g, int s_max) {
 // Most h_in slices per tile: slices of at least 512 rows, at most 8.
 int ks_max_for(int h_in) { return std::max(1, std::min(8, h_in / 512)); }
 
-// plora_apply runs as one launch for batches of up to kFusedTokens tokens;
-// plora_shrink then takes one h_in slice, so that its v carries the very
-// bits the fused launch computes.
+// plora_apply runs as one launch for batches of up to kFusedTokens tokens.
 bool fused_for(int32_t T) { return T <= kFusedTokens; }
 
-size_t workspace_bytes(int32_t T, const plora_adapters* ad) {
-  if (!ad || T <= 0 || ad->h_in <= 0 || ad->max_rank <= 0) return 0;
-  return (size_t)ks_max_for(ad->h_in) * T * ad->max_rank * sizeof(float);
+// Slices per tile of the one-launch form: kSlotTarget work groups over the
+// most tiles the batch can produce (rounded up to 8), to nearest, within
+// [1, min(ks_max, js_max)]; 1 when the tile slots outnumber the exchange
+// regions.  A function of the shapes alone (not of the device), so that the
+// workspace size is too.  plora_shrink and plora_expand take the same
+// slices for such batches, so their results carry the very bits of the
+// one-launch apply.
+int fused_slices(int32_t tile_cap, int32_t h_in, int32_t h_out) {
+  const int cap8 = (tile_cap + 7) & ~7;
+  if (cap8 <= 0 || cap8 > kXSlots) return 1;
+  const int lim = std::min(ks_max_for(h_in), std::max(1, h_out / kMinSlice));
+  return std::max(1, std::min(lim, (kSlotTarget + cap8 / 2) / cap8));
 }
+
+// Workspace sections, each 256-byte aligned: the epochs of the exchange's
+// tile slots (64-bit, kXSlots of them), the exchange regions of the
+// one-launch form (kSlotWords 64-bit words for each of the first
+// min(cap8, kXSlots) tile slots), then the partial sums of v of the
+// two-launch form and plora_shrink (fp32 [ks_max][T][max_rank]).  The
+// epochs and each slot's region sit at the same offsets for every batch
+// size, rank and slice count, which the tags rely on; only the last
+// section's place and size follow the shapes.
+struct WsLayout {
+  size_t xep, xw, vpart, total;
+};
+
+inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+WsLayout ws_layout(int32_t T, const plora_adapters* ad) {
+  WsLayout l{0, 0, 0, 0};
+  if (!ad || T <= 0 || ad->h_in <= 0 || ad->max_rank <= 0) return l;
+  const size_t nvp = (size_t)ks_max_for(ad->h_in) * T * ad->max_rank * sizeof(float);
+  const int32_t tcap = plora_tile_capacity(T, ad->n_adapters);
+  const size_t slots = (size_t)std::min(kXSlots, std::max(8, (tcap + 7) & ~7));
+  l.xep = 0;
+  l.xw = align256((size_t)kXSlots * sizeof(uint64_t));
+  l.vpart = align256(l.xw + slots * kSlotWords * sizeof(uint64_t));
+  l.total = align256(l.vpart + nvp);
+  return l;
+}
+
+size_t workspace_bytes(int32_t T, const plora_adapters* ad) { return ws_layout(T, ad).total; }
 
 plora_status check_adapters_host(const plora_adapters* ad) {
   if (!ad) return PLORA_ERR_INVALID_ARG;
@@ -1614,6 +1914,7 @@ plora_status check_segments_host(const plora_segments* seg, int32_t N) {
 void clear_stale_error() { (void)hipGetLastError(); }
 
 std::atomic<int32_t> g_last_hip_error{0};
+std::atomic<int32_t> g_exchange_polls{kSpinLimit};
 
 plora_status launch_status() {
   const hipError_t e = hipGetLastError();
@@ -1636,15 +1937,24 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   g.meta = seg->meta;
   g.T = seg->T; g.N = ad->n_adapters; g.h_in = ad->h_in; g.h_out = ad->h_out;
   g.max_rank = ad->max_rank; g.tile_cap = seg->tile_cap;
-  g.ks_max = fused_for(seg->T) ? 1 : ks_max_for(ad->h_in);
   g.js_max = std::max(1, ad->h_out / kMinSlice);
   g.slots = slots_for_device();
+  // one-launch batches take either S > 1 fixed slices per tile (exchange
+  // form) or one h_in slice and device-chosen column slices; the split calls
+  // take the same slices, so that they reproduce the apply's bits
+  const int fs = fused_for(seg->T) ? fused_slices(seg->tile_cap, ad->h_in, ad->h_out) : 0;
+  g.fixed_slices = fs > 1 ? fs : 0;
+  g.polls = g_exchange_polls.load();
+  g.ks_max = fs == 1 ? 1 : ks_max_for(ad->h_in);
   if (needs_ws && seg->T > 0) {
-    const size_t need = workspace_bytes(seg->T, ad);
+    const WsLayout l = ws_layout(seg->T, ad);
     if (!ws) return PLORA_ERR_INVALID_ARG;
     if (!aligned16(ws)) return PLORA_ERR_UNSUPPORTED;
-    if (ws_bytes < need) return PLORA_ERR_WORKSPACE_TOO_SMALL;
-    g.vpart = reinterpret_cast<float*>(ws);
+    if (ws_bytes < l.total) return PLORA_ERR_WORKSPACE_TOO_SMALL;
+    char* base = reinterpret_cast<char*>(ws);
+    g.vpart = reinterpret_cast<float*>(base + l.vpart);
+    g.xw = reinterpret_cast<uint64_t*>(base + l.xw);
+    g.xep = reinterpret_cast<uint64_t*>(base + l.xep);
   }
   return PLORA_OK;
 }
@@ -1658,7 +1968,7 @@ void allow_lds(const void* kernel, std::atomic<bool>& done) {
 }
 
 std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false},
-    g_lds_parts{false};
+    g_lds_cols{false}, g_lds_parts{false};
 
 template <class K>
 plora_status launch_items(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
@@ -1777,7 +2087,9 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
-  if (fused_for(seg->T)) return launch_items(apply_kernel, g_lds_apply, g, g.js_max, stream);
+  if (g.fixed_slices > 1) return launch_items(apply_kernel, g_lds_apply, g, g.js_max, stream);
+  if (fused_for(seg->T))
+    return launch_items(apply_cols_kernel, g_lds_cols, g, g.js_max, stream);
   st = launch_items(shrink_part_kernel, g_lds_shrink, g, g.ks_max, stream);
   if (st != PLORA_OK) return st;
   return launch_items(expand_kernel<true>, g_lds_parts, g, g.js_max, stream);
@@ -1835,5 +2147,9 @@ const char* plora_status_string(plora_status status) {
 }
 
 int32_t plora_debug_last_hip_error(void) { return g_last_hip_error.load(); }
+
+void plora_debug_set_exchange_polls(int32_t polls) {
+  g_exchange_polls.store(polls < 0 ? kSpinLimit : polls);
+}
 
 }  // extern "C"

@@ -29,7 +29,7 @@ PLORA_META_WORDS = 8
 EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
             "plora_check_adapters", "plora_status_string",
-            "plora_debug_last_hip_error")
+            "plora_debug_last_hip_error", "plora_debug_set_exchange_polls")
 
 
 class PloraError(RuntimeError):
@@ -85,6 +85,8 @@ def _load() -> ctypes.CDLL:
     L.plora_status_string.restype = ctypes.c_char_p
     L.plora_debug_last_hip_error.argtypes = []
     L.plora_debug_last_hip_error.restype = i32
+    L.plora_debug_set_exchange_polls.argtypes = [i32]
+    L.plora_debug_set_exchange_polls.restype = None
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
                "plora_expand", "plora_apply", "plora_check_adapters"):
         getattr(L, fn).restype = ctypes.c_int
@@ -140,6 +142,10 @@ def plora_apply(x: int, ldx: int, ad: plora_adapters, seg: plora_segments, y: in
                 ldy: int, ws: int, ws_bytes: int, stream: int) -> None:
     _ok("plora_apply", lib.plora_apply(x, ldx, ctypes.byref(ad), ctypes.byref(seg),
                                        y, ldy, ws, ws_bytes, stream))
+
+
+def plora_debug_set_exchange_polls(polls: int) -> None:
+    lib.plora_debug_set_exchange_polls(polls)
 
 
 def plora_check_adapters(ad: plora_adapters, stream: int) -> int:

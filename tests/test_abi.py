@@ -78,11 +78,29 @@ def _apply_status(ad=None, seg=None, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
                              ws_bytes, None)
 
 
+def _expected_ws(T, N, h_in, max_rank):
+    """The documented layout: 336 64-bit epochs, then one exchange region of
+    8 x 32 x 128 64-bit words per tile slot for min(336, max(8, cap8)) slots
+    (cap8 = the tile capacity rounded up to 8), then the partial sums of v
+    over min(8, h_in / 512) slices of h_in (fp32), each section 256-byte
+    aligned."""
+    up = lambda v: (v + 255) // 256 * 256
+    k = min(8, max(1, h_in // 512))
+    slots = min(336, max(8, (P.plora_tile_capacity(T, N) + 7) // 8 * 8))
+    return up(up(up(336 * 8) + slots * 8 * 32 * 128 * 8) + k * T * max_rank * 4)
+
+
 def test_workspace_size_and_checks():
-    # partial sums of v over min(8, h_in / 512) slices of h_in, fp32
     for h_in, k in [(256, 1), (1024, 2), (4096, 8), (32768, 8)]:
         ad = _ad(h_in=h_in, max_rank=16)
-        assert P.plora_workspace_bytes(100, ad) == k * 100 * 16 * 4
+        assert P.plora_workspace_bytes(100, ad) == _expected_ws(100, 4, h_in, 16)
+        assert P.plora_workspace_bytes(100, ad) >= k * 100 * 16 * 4
+    # the exchange regions stop growing at 336 tile slots
+    big = _ad(n_adapters=1000, h_in=4096, max_rank=16)
+    for T in (8, 64, 300, 1024, 16384):
+        assert P.plora_workspace_bytes(T, big) == _expected_ws(T, 1000, 4096, 16)
+    assert (P.plora_workspace_bytes(16384, big) - 8 * 16384 * 16 * 4
+            < 337 * 8 * 32 * 128 * 8 + 4096)
     ad = _ad()
     assert P.plora_workspace_bytes(0, ad) == 0
     assert P.lib.plora_workspace_init(None, 0, None) == P.PLORA_OK

@@ -306,6 +306,78 @@ def test_deterministic_and_workspace_reuse(P, name):
     assert all((o == outs[0]).all() for o in outs[1:])
 
 
+def test_exchange_fallback_meets_the_bars(P):
+    """Polls forced to 0: every one-launch item that does not find all its
+    partners' partial v on its first look computes v by itself.  That path
+    sums in another order, so it is checked against the oracle's bars, not
+    bit for bit against the exchanged result."""
+    for scale in ("parity", "paper"):
+        w = workload("decode", scale)
+        say(f"exchange fallback decode/{scale}")
+        run = Run(P, w).segment()
+        P.plora_debug_set_exchange_polls(0)
+        try:
+            y = run.apply()
+        finally:
+            P.plora_debug_set_exchange_polls(-1)
+        yref, yout = oracle_y(w)
+        check_y(y, yref, yout, w, strict_l2=(scale == "parity"))
+        # and the default again gives the exchanged (split-equal) bits
+        assert (run.apply() == run.expand(run.shrink())).all()
+
+
+def test_workspace_shared_across_batches_and_stacks(P):
+    """One workspace serving one-launch calls of varying batch size and of two
+    adapter stacks (ranks 16 and 64) in turn: its exchange regions and epochs
+    carry over from call to call, and stale words must never be taken."""
+    stacks = [workload("decode", "parity"), workload("large", "parity")]
+    ads = [P.Adapters.from_workload(w) for w in stacks]
+    ws = P.Workspace(256, ads[1])
+    assert ws.nbytes >= P.plora_workspace_bytes(256, ads[0].struct)
+    rng = np.random.default_rng(5)
+    for k, T in enumerate((64, 16, 256, 64, 8, 128, 64, 200)):
+        j = k % 2
+        w = stacks[j]
+        idx = W.zipf_ids(rng, T, w.n_adapters, 1.0)
+        ww = W.with_idx(w, idx)
+        say(f"shared workspace call {k}: stack {j} T={T}")
+        segs = P.Segments(T, w.n_adapters)
+        P.segment(dev(idx), segs)
+        x = dev(np.ascontiguousarray(ww.x).view(np.int16))
+        y = dev(np.ascontiguousarray(ww.y_base).view(np.int16))
+        P.apply(x, ads[j], segs, y, ws)
+        torch.cuda.synchronize()
+        yref, yout = oracle_y(ww)
+        check_y(bits16(y), yref, yout, ww, strict_l2=True)
+
+
+def test_apply_graph_replay(P):
+    """plora_apply captured in a graph and replayed (the exchange's epochs
+    live on the device, so every replay gets fresh tags), with eager calls
+    between the replays and new x each time; every replay equals the eager
+    call on the same inputs bit for bit."""
+    w = workload("decode", "parity")
+    run = Run(P, w).segment()
+    rng = np.random.default_rng(9)
+    xs = [run.x.clone()] + [run.x[torch.from_numpy(rng.permutation(w.T)).cuda()].clone()
+                            for _ in range(2)]
+    y = dev(run.y0.view(np.int16))
+    run.apply()                                  # warm-up outside the capture
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        P.apply(run.x, run.ad, run.segs, y, run.ws)
+    for k, xk in enumerate(xs * 2):
+        say(f"graph replay {k}")
+        run.x.copy_(xk)
+        y.copy_(dev(run.y0.view(np.int16)))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = bits16(y)[:, :w.h_out]
+        want = run.apply()                       # eager, same inputs
+        assert (got == want).all(), k
+
+
 def test_token_permutation_bitwise(P):
     w = workload("decode", "parity")
     p = np.random.default_rng(8).permutation(w.T)
