@@ -10,7 +10,9 @@ the adapter stack, so that an adapter's bytes are never still sitting in the
 projection's stack only after every other LoRA projection of every layer).
 
 Prints ONE JSON line.  ``value`` is whole-job tokens/s over the timed steps
-(wall clock, segment + apply).  ``roofline`` prices the dominant kernel,
+(wall clock, segment + apply), the K steps launched as one captured HIP graph
+(``--eager``: one launch per kernel from Python; the eager time is reported
+too).  ``roofline`` prices the dominant kernel,
 plora_apply: algorithmic bytes per call (distinct adapters' A_i and B_i,
 2 r_i (h_in + h_out) bytes each, plus x read, y read and written, and the
 token permutation) over its average duration: K calls issued back to back
@@ -50,6 +52,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
+    ap.add_argument("--eager", action="store_true",
+                    help="time the steps as individual launches instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run 10 plain device copies of MIB MiB (the reference "
                          "kernel for scaling HBM byte counters) and exit")
@@ -181,7 +185,25 @@ def main():
     for k in range(K):
         step(args.warmup + k, evs[k])
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    wall_eager = time.perf_counter() - t0
+    wall = wall_eager
+
+    # ---- the same K steps launched as one HIP graph ------------------------------
+    # At decode size a step's two kernels take less GPU time than Python needs
+    # to issue them, so the eager loop measures the host.  The K steps (same
+    # draws, same stack replicas) are captured once and the graph is replayed:
+    # once untimed, then once timed.
+    if not args.eager:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for k in range(K):
+                step(args.warmup + k)
+        graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        graph.replay()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
 
     apply_ms = np.array([a.elapsed_time(b) for a, b in evs])
     ks = [(args.warmup + k) % len(draws) for k in range(K)]
@@ -279,6 +301,8 @@ def main():
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": round(wall / K * 1e3, 5),
+        "launch": "eager" if args.eager else "hip graph of the K steps",
+        "ms_per_step_eager": round(wall_eager / K * 1e3, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
