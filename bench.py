@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-ceiling", action="store_true")
+    ap.add_argument("--projections", type=int, default=1,
+                    help="LoRA-injected projections of one layer sharing x, applied "
+                         "by one plora_apply_multi call (1: plora_apply)")
     ap.add_argument("--eager", action="store_true",
                     help="time the steps as individual launches instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -133,43 +136,64 @@ def main():
     seed = 1000 + W.CONFIG_NAMES.index(name)
     w = W.make_workload(name)
     N = w.n_adapters
+    n_proj = args.projections
+    # the projections of one layer that share x (projection 0 is the config's
+    # own workload); one projection is the plain plora_apply
+    wps = [w] if n_proj == 1 else W.make_projections(name, n_proj=n_proj)
+    if len(wps) != n_proj:
+        print(f"bench.py: config {name} defines {len(wps)} projections", file=sys.stderr)
+        sys.exit(2)
 
     # ---- token-to-adapter draws -------------------------------------------------
     draws = [W.draw_idx(name, seed, d) for d in range(args.draws)]
     Tmax = max(d.size for d in draws)
-    act_bytes = lambda T: T * (2 * w.h_in + 4 * w.h_out) + 4 * T
-    ad_bytes = [W.adapter_bytes(w.ranks, d, w.h_in, w.h_out, N) for d in draws]
+    act_bytes = lambda T: T * (2 * w.h_in + sum(4 * wp.h_out for wp in wps)) + 4 * T
+    ad_bytes = [sum(W.adapter_bytes(wp.ranks, d, wp.h_in, wp.h_out, N) for wp in wps)
+                for d in draws]
     tot_bytes = [a + act_bytes(d.size) for a, d in zip(ad_bytes, draws)]
 
     # ---- device buffers -----------------------------------------------------------
-    base = P.Adapters.from_workload(w, device=dev)
-    stack_bytes = 2 * (base.A.numel() + base.B.numel())
+    bases = [P.Adapters.from_workload(wp, device=dev) for wp in wps]
+    stack_bytes = sum(2 * (b.A.numel() + b.B.numel()) for b in bases)
     R = args.replicas
     if R <= 0:
         per_step = max(1, int(np.mean(ad_bytes)))
         R = max(2, min(64, math.ceil(3 * MALL_BYTES / per_step)))
         R = max(1, min(R, int((96 << 30) // max(stack_bytes, 1))))
-    reps = [base]
+    reps = [bases]
     for _ in range(R - 1):
-        reps.append(P.Adapters(base.A.clone(), base.B.clone(), base.a_off, base.b_off,
-                               base.ranks, base.scales, w.h_in, w.h_out, base.max_rank))
+        reps.append([P.Adapters(b.A.clone(), b.B.clone(), b.a_off, b.b_off, b.ranks, b.scales,
+                                b.h_in, b.h_out, b.max_rank) for b in bases])
     xw = w if Tmax == w.T else W.with_idx(w, np.zeros(Tmax, np.int32))
     x = torch.from_numpy(xw.x).view(torch.int16).to(dev)
-    y_host = np.zeros((Tmax, w.h_out), np.uint16)
-    n = min(Tmax, w.T)
-    y_host[:n] = w.y_base[:n]
-    y = torch.from_numpy(y_host).view(torch.int16).to(dev)
-    ws = P.Workspace(Tmax, base)
+    ys = []
+    for wp in wps:
+        y_host = np.zeros((Tmax, wp.h_out), np.uint16)
+        n = min(Tmax, wp.T)
+        y_host[:n] = wp.y_base[:n]
+        ys.append(torch.from_numpy(y_host).view(torch.int16).to(dev))
+    ws = P.Workspace(Tmax, bases if n_proj > 1 else bases[0])
     idx_dev = [torch.from_numpy(d).to(dev) for d in draws]
     segs = [P.Segments(d.size, N, device=dev) for d in draws]
 
-    def step(k, ev=None):
+    def apply_call(k, separate=False):
         d = k % len(draws)
         T = draws[d].size
+        rp = reps[k % R]
+        if n_proj == 1:
+            P.apply(x[:T], rp[0], segs[d], ys[0][:T], ws)
+        elif separate:
+            for q in range(n_proj):
+                P.apply(x[:T], rp[q], segs[d], ys[q][:T], ws)
+        else:
+            P.apply_multi(x[:T], rp, segs[d], [yq[:T] for yq in ys], ws)
+
+    def step(k, ev=None):
+        d = k % len(draws)
         P.segment(idx_dev[d], segs[d])
         if ev is not None:
             ev[0].record()
-        P.apply(x[:T], reps[k % R], segs[d], y[:T], ws)
+        apply_call(k)
         if ev is not None:
             ev[1].record()
 
@@ -219,20 +243,27 @@ def main():
     b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     b0.record()
     for k in range(K):
-        d = k % len(draws)
-        P.apply(x[:draws[d].size], reps[k % R], segs[d], y[:draws[d].size], ws)
+        apply_call(k)
     b1.record()
     torch.cuda.synchronize()
     apply_s = b0.elapsed_time(b1) / 1e3
+    separate_s = None
+    if n_proj > 1:                           # the same work as one call per projection
+        b0.record()
+        for k in range(K):
+            apply_call(k, separate=True)
+        b1.record()
+        torch.cuda.synchronize()
+        separate_s = b0.elapsed_time(b1) / 1e3
     bytes_total = sum(tot_bytes[k % len(draws)] for k in range(K))
     bytes_adapter = sum(ad_bytes[k % len(draws)] for k in range(K))
     achieved = bytes_total / apply_s / 1e9
-    traffic = measured_traffic(name)
+    traffic = measured_traffic(name) if n_proj == 1 else None
     adapter_gbps = bytes_adapter / apply_s / 1e9
 
     # ---- same-footprint plain-read ceiling -------------------------------------
     ceiling = None
-    if not args.no_ceiling:
+    if not args.no_ceiling and n_proj == 1:
         import ctypes
         from paper_2608_05483_amd import build as B
         pl = ctypes.CDLL(B.PROBE_LIB)
@@ -247,7 +278,7 @@ def main():
 
         def probe(k):
             d = k % len(draws)
-            rp = reps[k % R]
+            rp = reps[k % R][0]
             rc = pl.plora_probe_read(rp.A.data_ptr(), rp.B.data_ptr(), rp.a_off.data_ptr(),
                                      rp.b_off.data_ptr(), rp.ranks.data_ptr(),
                                      uniq[d].data_ptr(), uniq[d].numel(), w.h_in, w.h_out,
@@ -282,8 +313,10 @@ def main():
             d = draws[n_done % len(draws)]
             wd = w if d.size == w.T else W.with_idx(w, d)
             t1 = time.perf_counter()
-            oracle.apply(wd.x, d, w.A, w.a_off, w.B, w.b_off, w.ranks, w.scales,
-                         wd.y_base, w.h_in, w.h_out, n_threads=cores)
+            for wp in wps:
+                oracle.apply(wd.x, d, wp.A, wp.a_off, wp.B, wp.b_off, wp.ranks, wp.scales,
+                             np.zeros((d.size, wp.h_out), np.uint16), w.h_in, wp.h_out,
+                             n_threads=cores)
             t_cpu += time.perf_counter() - t1
             toks += d.size
             n_done += 1
@@ -308,8 +341,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(name, c), "T": int(Tmax), "h_in": w.h_in,
-                   "h_out": w.h_out, "max_rank": w.max_rank, "n_adapters": N,
+        "config": {"workload": describe(name, c) + (
+                       "" if n_proj == 1 else
+                       f"; {n_proj} projections sharing x, h_out "
+                       f"{[wp.h_out for wp in wps]}, one plora_apply_multi call"),
+                   "T": int(Tmax), "h_in": w.h_in,
+                   "h_out": w.h_out if n_proj == 1 else [wp.h_out for wp in wps],
+                   "max_rank": w.max_rank, "n_adapters": N,
                    "draws": len(draws), "stack_replicas": R},
         "adapter_GBps": round(adapter_gbps, 1),
         "adapter_frac_of_peak": round(adapter_gbps / HBM_PEAK_GBPS, 4),
@@ -324,6 +362,8 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic},
         "read_ceiling": ceiling,
+        "separate_calls_us": (None if separate_s is None
+                              else round(separate_s / K * 1e6, 3)),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -101,6 +101,8 @@ typedef enum {
 #define PLORA_MAX_TOKENS 16384
 /* Tokens per work tile; a segment longer than this is split into tiles. */
 #define PLORA_TILE_TOKENS 32
+/* Most projections one plora_apply_multi call serves. */
+#define PLORA_MAX_PROJECTIONS 8
 /* Entries of plora_segments.meta. */
 #define PLORA_META_WORDS 8
 
@@ -243,6 +245,42 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx,
                          const plora_adapters* ad, const plora_segments* seg,
                          uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+
+/*
+ * The apply for several projections of one layer that read the same input x
+ * and the same token batch (the paper attaches LoRA adapters to the query,
+ * key, value and output projections and the FFN, section VII-A; section II-A
+ * gives each its own A and B): for p < n_proj,
+ *   ys[p][t] = bf16(ys[p][t] + s_i^p (x[t] A_i^p) B_i^p),  i = idx[t],
+ * with ads[p] the adapter stack of projection p (host array of n_proj
+ * structs; every stack has the same n_adapters and h_in, while h_out and
+ * the ranks may differ), ys a host array of n_proj device pointers and ldys
+ * a host array of their leading dimensions.  seg, ws and stream as for
+ * plora_apply; ws must hold plora_workspace_bytes_multi(T, ads, n_proj)
+ * bytes, zeroed once before its first use.  Batches small enough for the
+ * split exchange of plora_apply run all projections in one launch (their
+ * tiles share the work groups, and each tile gets fewer slices than one
+ * projection's alone would, so the bits can differ from separate
+ * plora_apply calls while meeting the same bounds); other batches run
+ * plora_apply once per projection.  Bitwise deterministic (with the same
+ * exception as plora_apply).  Outputs must not overlap x or each other.
+ * PLORA_ERR_INVALID_ARG for null arrays, n_proj < 1, stacks whose
+ * n_adapters or h_in differ, or a leading dimension below its width;
+ * PLORA_ERR_UNSUPPORTED for n_proj > PLORA_MAX_PROJECTIONS and the
+ * alignment rules of plora_apply.
+ */
+plora_status plora_apply_multi(const uint16_t* x, int64_t ldx,
+                               const plora_adapters* ads, int32_t n_proj,
+                               const plora_segments* seg,
+                               uint16_t* const* ys, const int64_t* ldys,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Host.  Workspace bytes plora_apply_multi needs for a batch of up to T
+ * tokens over these n_proj stacks: the layout of plora_workspace_bytes with
+ * n_proj cap8 tile slots (still at most 336) and the largest partial-sum
+ * section of the stacks; 0 for bad arguments or T <= 0.  It also serves
+ * plora_apply and plora_shrink on any one of the stacks. */
+size_t plora_workspace_bytes_multi(int32_t T, const plora_adapters* ads, int32_t n_proj);
 
 /*
  * Host, synchronous (copies ranks and offsets to the host and waits on

@@ -217,3 +217,16 @@ def apply_grouped(x, idx, A, a_off, B, b_off, ranks, scales, y_base,
     if rc != 0:
         raise RuntimeError("oracle_apply_grouped failed")
     return yref, yout
+
+
+def apply_multi(x, idx, stacks, y_bases, h_in: int, n_threads: int = 1):
+    """The apply for several projections of one layer that read the same x
+    and token ids (section VII-A attaches adapters to the attention
+    projections and the FFN; section II-A gives each its own A and B): each
+    projection is the single-projection definition on its own stack.
+
+    stacks: per projection a tuple (A, a_off, B, b_off, ranks, scales, h_out);
+    y_bases: per projection its y_base.  Returns a list of (yref, y bf16)."""
+    return [apply(x, idx, A, a_off, B, b_off, ranks, scales, yb, h_in, h_out,
+                  n_threads=n_threads)
+            for (A, a_off, B, b_off, ranks, scales, h_out), yb in zip(stacks, y_bases)]

@@ -1656,33 +1656,28 @@ __device__ __forceinline__ void plain_v(const ApplyArgs& g, const Tile& t, const
   lds_sync();
 }
 
-// plora_apply as one launch, tiles in S > 1 slices: item blockIdx.x =
-// u S + s is slice s of tile u (S = g.fixed_slices, chosen on the host, so
-// the item needs no count from the device): the shrink of h_in rows
-// [s KR, (s+1) KR), the exchange of partial v with the tile's other items,
-// and the expand of y columns [s W, (s+1) W), whose first loads of B_i and
-// y are issued before the exchange waits.  A tile's items are neighbours
-// in the grid, so the work groups a tile waits on are dispatched with it.
-// If the exchange times out, plain_v computes v here.
-__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
-  extern __shared__ __align__(16) unsigned char apply_lds[];
-  __shared__ ItemStash stash;
+// One item of the one-launch form with S = g.fixed_slices > 1 slices per
+// tile: slice s of tile u, exchanging through tile slot `slot` (its region
+// and epoch in the workspace): the shrink of h_in rows [s KR, (s+1) KR),
+// the exchange of partial v with the tile's other items, and the expand of
+// y columns [s W, (s+1) W), whose first loads of B_i and y are issued before
+// the exchange waits.  If the exchange times out, plain_v computes v here.
+__device__ __forceinline__ void apply_item(const ApplyArgs& g, int u, int s, int slot,
+                                           ItemStash& stash, unsigned char* lds) {
   {
-    const int S = g.fixed_slices;
-    const int u = (int)blockIdx.x / S, s = (int)blockIdx.x - u * S;
     // the slot's epoch is requested together with the tile record (the host
-    // made sure u < kXSlots)
-    const uint64_t ep = u < g.tile_cap ? xload(g.xep + u) : 0;
+    // made sure slot < kXSlots)
+    const uint64_t ep = u < g.tile_cap ? xload(g.xep + slot) : 0;
     Tile t;
     int my_tok;
     if (!load_tile(g, u, t, my_tok)) return;
     if (threadIdx.x == 0) {
       stash.a = t.a; stash.p0 = t.p0; stash.L = t.L; stash.r = t.r; stash.s = t.s;
-      stash.u = u; stash.slice = s; stash.Ai = t.Ai; stash.Bi = t.Bi; stash.ep = ep;
+      stash.u = slot; stash.slice = s; stash.Ai = t.Ai; stash.Bi = t.Bi; stash.ep = ep;
     }
-    (void)tile_prologue(g, my_tok, apply_lds);     // ends with a barrier
+    (void)tile_prologue(g, my_tok, lds);           // ends with a barrier
   }
-  const Smem sm = carve(apply_lds, g.max_rank);
+  const Smem sm = carve(lds, g.max_rank);
   const int S = g.fixed_slices;
   const int KR = ((g.h_in + S - 1) / S + 63) & ~63;
   {
@@ -1695,14 +1690,14 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   }
   {
     Tile t = unstash(&stash);
-    const int s = uni(stash.slice);
+    const int sl = uni(stash.slice);
     const int W = ((g.h_out + S - 1) / S + 15) & ~15;
     t.k0 = 0;
     t.k1 = g.h_in;
-    t.j0 = s * W;
+    t.j0 = sl * W;
     t.j1 = min(g.h_out, t.j0 + W);
-    const Xchg xc{s, S, KR, (uint32_t)(stash.ep + 1), g.xw + (int64_t)uni(stash.u) * kSlotWords,
-                  g.polls};
+    const Xchg xc{sl, S, KR, (uint32_t)(stash.ep + 1),
+                  g.xw + (int64_t)uni(stash.u) * kSlotWords, g.polls};
     expand_hooked(g, t, sm, [&] {
       if (!exchange_v(t, sm, xc)) plain_v(g, t, sm);
     });
@@ -1710,6 +1705,57 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   if (threadIdx.x == 0)
     __hip_atomic_fetch_max(g.xep + stash.u, stash.ep + 1, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// plora_apply as one launch, tiles in S > 1 slices: item blockIdx.x = u S + s
+// (S chosen on the host, so the item needs no count from the device), tile
+// slot u.  A tile's items are neighbours in the grid, so the work groups a
+// tile waits on are dispatched with it.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  const int S = g.fixed_slices;
+  const int u = (int)blockIdx.x / S, s = (int)blockIdx.x - u * S;
+  apply_item(g, u, s, u, stash, apply_lds);
+}
+
+// The per-projection part of a multi-projection apply (see plora_apply_multi).
+struct ProjArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  int64_t a_len, b_len;
+  const int64_t* a_off;
+  const int64_t* b_off;
+  const int32_t* ranks;
+  const float* scales;
+  uint16_t* y;
+  int64_t ldy;
+  int32_t h_out, max_rank;
+};
+
+struct MultiArgs {
+  ApplyArgs g;            // shared: x, the segments, the workspace, the plan
+  ProjArgs proj[PLORA_MAX_PROJECTIONS];
+  int32_t n_proj;
+  int32_t cap8;           // tile capacity rounded up to 8
+};
+
+// Several projections in one launch, S > 1 slices per tile: item
+// blockIdx.x = (p cap8 + u) S + s is slice s of tile u of projection p,
+// exchanging through tile slot p cap8 + u.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_multi_kernel(MultiArgs m) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  const int S = m.g.fixed_slices;
+  const int slot = (int)blockIdx.x / S, s = (int)blockIdx.x - slot * S;
+  const int p = slot / m.cap8, u = slot - p * m.cap8;
+  if (p >= m.n_proj) return;
+  ApplyArgs g = m.g;
+  const ProjArgs& q = m.proj[p];
+  g.A = q.A; g.B = q.B; g.a_len = q.a_len; g.b_len = q.b_len;
+  g.a_off = q.a_off; g.b_off = q.b_off; g.ranks = q.ranks; g.scales = q.scales;
+  g.y = q.y; g.ldy = q.ldy; g.h_out = q.h_out; g.max_rank = q.max_rank;
+  apply_item(g, u, s, slot, stash, apply_lds);
 }
 
 // plora_apply as one launch, one slice per tile in h_in: item (tile,
@@ -1842,11 +1888,20 @@ bool fused_for(int32_t T) { return T <= kFusedTokens; }
 // workspace size is too.  plora_shrink and plora_expand take the same
 // slices for such batches, so their results carry the very bits of the
 // one-launch apply.
+// (For n projections in one launch, plora_apply_multi, the tile slots of
+// all of them count: n cap8 of them, and the limit is the smallest
+// projection's.)
+int fused_slices_for(int slots8, int lim) {
+  if (slots8 <= 0 || slots8 > kXSlots) return 1;
+  return std::max(1, std::min(lim, (kSlotTarget + slots8 / 2) / slots8));
+}
+
+int slice_limit(int32_t h_in, int32_t h_out) {
+  return std::min(ks_max_for(h_in), std::max(1, h_out / kMinSlice));
+}
+
 int fused_slices(int32_t tile_cap, int32_t h_in, int32_t h_out) {
-  const int cap8 = (tile_cap + 7) & ~7;
-  if (cap8 <= 0 || cap8 > kXSlots) return 1;
-  const int lim = std::min(ks_max_for(h_in), std::max(1, h_out / kMinSlice));
-  return std::max(1, std::min(lim, (kSlotTarget + cap8 / 2) / cap8));
+  return fused_slices_for((tile_cap + 7) & ~7, slice_limit(h_in, h_out));
 }
 
 // Workspace sections, each 256-byte aligned: the epochs of the exchange's
@@ -1863,12 +1918,18 @@ struct WsLayout {
 
 inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-WsLayout ws_layout(int32_t T, const plora_adapters* ad) {
+// n adapter stacks (the projections of plora_apply_multi; n = 1 otherwise)
+// sharing the batch: n cap8 tile slots, and the largest partial-sum section.
+WsLayout ws_layout(int32_t T, const plora_adapters* ad, int n = 1) {
   WsLayout l{0, 0, 0, 0};
-  if (!ad || T <= 0 || ad->h_in <= 0 || ad->max_rank <= 0) return l;
-  const size_t nvp = (size_t)ks_max_for(ad->h_in) * T * ad->max_rank * sizeof(float);
+  if (!ad || T <= 0 || n < 1) return l;
+  size_t nvp = 0;
+  for (int p = 0; p < n; ++p) {
+    if (ad[p].h_in <= 0 || ad[p].max_rank <= 0) return l;
+    nvp = std::max(nvp, (size_t)ks_max_for(ad[p].h_in) * T * ad[p].max_rank * sizeof(float));
+  }
   const int32_t tcap = plora_tile_capacity(T, ad->n_adapters);
-  const size_t slots = (size_t)std::min(kXSlots, std::max(8, (tcap + 7) & ~7));
+  const size_t slots = (size_t)std::min(kXSlots, std::max(8, n * ((tcap + 7) & ~7)));
   l.xep = 0;
   l.xw = align256((size_t)kXSlots * sizeof(uint64_t));
   l.vpart = align256(l.xw + slots * kSlotWords * sizeof(uint64_t));
@@ -1968,7 +2029,7 @@ void allow_lds(const void* kernel, std::atomic<bool>& done) {
 }
 
 std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false},
-    g_lds_cols{false}, g_lds_parts{false};
+    g_lds_cols{false}, g_lds_parts{false}, g_lds_multi{false};
 
 template <class K>
 plora_status launch_items(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
@@ -2093,6 +2154,76 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   st = launch_items(shrink_part_kernel, g_lds_shrink, g, g.ks_max, stream);
   if (st != PLORA_OK) return st;
   return launch_items(expand_kernel<true>, g_lds_parts, g, g.js_max, stream);
+}
+
+size_t plora_workspace_bytes_multi(int32_t T, const plora_adapters* ads, int32_t n_proj) {
+  if (!ads || n_proj < 1 || n_proj > PLORA_MAX_PROJECTIONS) return 0;
+  return ws_layout(T, ads, n_proj).total;
+}
+
+plora_status plora_apply_multi(const uint16_t* x, int64_t ldx, const plora_adapters* ads,
+                               int32_t n_proj, const plora_segments* seg,
+                               uint16_t* const* ys, const int64_t* ldys, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  if (!ads || !ys || !ldys || n_proj < 1) return PLORA_ERR_INVALID_ARG;
+  if (n_proj > PLORA_MAX_PROJECTIONS) return PLORA_ERR_UNSUPPORTED;
+  for (int p = 0; p < n_proj; ++p) {
+    const plora_status st = check_adapters_host(&ads[p]);
+    if (st != PLORA_OK) return st;
+    if (ads[p].n_adapters != ads[0].n_adapters || ads[p].h_in != ads[0].h_in)
+      return PLORA_ERR_INVALID_ARG;
+  }
+  plora_status st = check_segments_host(seg, ads[0].n_adapters);
+  if (st != PLORA_OK) return st;
+  if (seg->T == 0) return PLORA_OK;
+  if (!x || ldx < ads[0].h_in) return PLORA_ERR_INVALID_ARG;
+  if ((ldx & 7) || !aligned16(x)) return PLORA_ERR_UNSUPPORTED;
+  int lim = PLORA_MAX_RANK, max_rank = 0;
+  for (int p = 0; p < n_proj; ++p) {
+    if (!ys[p] || ldys[p] < ads[p].h_out) return PLORA_ERR_INVALID_ARG;
+    if ((ldys[p] & 7) || !aligned16(ys[p])) return PLORA_ERR_UNSUPPORTED;
+    lim = std::min(lim, slice_limit(ads[p].h_in, ads[p].h_out));
+    max_rank = std::max(max_rank, ads[p].max_rank);
+  }
+  const WsLayout l = ws_layout(seg->T, ads, n_proj);
+  if (!ws) return PLORA_ERR_INVALID_ARG;
+  if (!aligned16(ws)) return PLORA_ERR_UNSUPPORTED;
+  if (ws_bytes < l.total) return PLORA_ERR_WORKSPACE_TOO_SMALL;
+  const int cap8 = (seg->tile_cap + 7) & ~7;
+  const int S = fused_for(seg->T) ? fused_slices_for(n_proj * cap8, lim) : 1;
+  if (S <= 1) {
+    // one projection after another (the launch overheads are small next to
+    // batches this large)
+    for (int p = 0; p < n_proj; ++p) {
+      st = plora_apply(x, ldx, &ads[p], seg, ys[p], ldys[p], ws, ws_bytes, stream);
+      if (st != PLORA_OK) return st;
+    }
+    return PLORA_OK;
+  }
+  MultiArgs m;
+  memset(&m, 0, sizeof m);
+  st = prepare(&ads[0], seg, ws, ws_bytes, m.g, true);
+  if (st != PLORA_OK) return st;
+  char* base = reinterpret_cast<char*>(ws);
+  m.g.vpart = reinterpret_cast<float*>(base + l.vpart);
+  m.g.x = x;
+  m.g.ldx = ldx;
+  m.g.fixed_slices = S;
+  m.n_proj = n_proj;
+  m.cap8 = cap8;
+  for (int p = 0; p < n_proj; ++p) {
+    ProjArgs& q = m.proj[p];
+    q.A = ads[p].A; q.B = ads[p].B; q.a_len = ads[p].a_len; q.b_len = ads[p].b_len;
+    q.a_off = ads[p].a_off; q.b_off = ads[p].b_off; q.ranks = ads[p].ranks;
+    q.scales = ads[p].scales; q.y = ys[p]; q.ldy = ldys[p]; q.h_out = ads[p].h_out;
+    q.max_rank = ads[p].max_rank;
+  }
+  const size_t lds = smem_bytes(ads[0].h_in, max_rank);
+  if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(apply_multi_kernel), g_lds_multi);
+  clear_stale_error();
+  hipLaunchKernelGGL(apply_multi_kernel, dim3((unsigned)(n_proj * cap8 * S)), dim3(kNT), lds,
+                     stream, m);
+  return launch_status();
 }
 
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,

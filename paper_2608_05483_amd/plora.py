@@ -25,9 +25,11 @@ PLORA_MAX_RANK = 128
 PLORA_MAX_TOKENS = 16384
 PLORA_TILE_TOKENS = 32
 PLORA_META_WORDS = 8
+PLORA_MAX_PROJECTIONS = 8
 
 EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
+            "plora_apply_multi", "plora_workspace_bytes_multi",
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls")
 
@@ -80,6 +82,10 @@ def _load() -> ctypes.CDLL:
     L.plora_shrink.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_expand.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_apply.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_apply_multi.argtypes = [P, i64, AD, i32, SG, ctypes.POINTER(P),
+                                    ctypes.POINTER(i64), P, sz, P]
+    L.plora_workspace_bytes_multi.argtypes = [i32, AD, i32]
+    L.plora_workspace_bytes_multi.restype = sz
     L.plora_check_adapters.argtypes = [AD, ctypes.POINTER(i32), P]
     L.plora_status_string.argtypes = [ctypes.c_int]
     L.plora_status_string.restype = ctypes.c_char_p
@@ -88,7 +94,7 @@ def _load() -> ctypes.CDLL:
     L.plora_debug_set_exchange_polls.argtypes = [i32]
     L.plora_debug_set_exchange_polls.restype = None
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
-               "plora_expand", "plora_apply", "plora_check_adapters"):
+               "plora_expand", "plora_apply", "plora_apply_multi", "plora_check_adapters"):
         getattr(L, fn).restype = ctypes.c_int
     return L
 
@@ -142,6 +148,30 @@ def plora_apply(x: int, ldx: int, ad: plora_adapters, seg: plora_segments, y: in
                 ldy: int, ws: int, ws_bytes: int, stream: int) -> None:
     _ok("plora_apply", lib.plora_apply(x, ldx, ctypes.byref(ad), ctypes.byref(seg),
                                        y, ldy, ws, ws_bytes, stream))
+
+
+def _stack_array(ads):
+    arr = (plora_adapters * len(ads))()
+    for i, a in enumerate(ads):
+        arr[i] = a
+    return arr
+
+
+def plora_workspace_bytes_multi(T: int, ads) -> int:
+    """ads: a sequence of plora_adapters structs."""
+    return int(lib.plora_workspace_bytes_multi(T, _stack_array(ads), len(ads)))
+
+
+def plora_apply_multi(x: int, ldx: int, ads, seg: plora_segments, ys, ldys, ws: int,
+                      ws_bytes: int, stream: int) -> None:
+    """ads: plora_adapters structs; ys, ldys: device pointers and leading
+    dimensions, one per projection."""
+    n = len(ads)
+    yarr = (ctypes.c_void_p * n)(*ys)
+    larr = (ctypes.c_int64 * n)(*ldys)
+    _ok("plora_apply_multi", lib.plora_apply_multi(x, ldx, _stack_array(ads), n,
+                                                   ctypes.byref(seg), yarr, larr, ws,
+                                                   ws_bytes, stream))
 
 
 def plora_debug_set_exchange_polls(polls: int) -> None:
@@ -226,12 +256,15 @@ class Segments:
 
 
 class Workspace:
-    """Zero-initialised workspace of plora_workspace_bytes(T, stack) bytes
-    (currently 0: the pointer passed is then NULL)."""
+    """Zero-initialised workspace of plora_workspace_bytes(T, stack) bytes, or
+    plora_workspace_bytes_multi(T, stacks) for a list of stacks."""
 
-    def __init__(self, T: int, ad: Adapters, device="cuda", stream=None):
+    def __init__(self, T: int, ad, device="cuda", stream=None):
         import torch
-        self.nbytes = plora_workspace_bytes(T, ad.struct)
+        if isinstance(ad, (list, tuple)):
+            self.nbytes = plora_workspace_bytes_multi(T, [a.struct for a in ad])
+        else:
+            self.nbytes = plora_workspace_bytes(T, ad.struct)
         self.buf = None
         if self.nbytes:
             self.buf = torch.empty(self.nbytes, dtype=torch.uint8, device=device)
@@ -260,3 +293,10 @@ def expand(v, ad: Adapters, segs: Segments, y, stream=None) -> None:
 def apply(x, ad: Adapters, segs: Segments, y, ws: Workspace, stream=None) -> None:
     plora_apply(x.data_ptr(), x.stride(0), ad.struct, segs.struct, y.data_ptr(),
                 y.stride(0), ws.ptr, ws.nbytes, _stream(stream))
+
+
+def apply_multi(x, ads, segs: Segments, ys, ws: Workspace, stream=None) -> None:
+    """ads: Adapters, one per projection; ys: their output tensors."""
+    plora_apply_multi(x.data_ptr(), x.stride(0), [a.struct for a in ads], segs.struct,
+                      [y.data_ptr() for y in ys], [y.stride(0) for y in ys], ws.ptr,
+                      ws.nbytes, _stream(stream))

@@ -204,14 +204,20 @@ def fill_adapters(A: np.ndarray, B: np.ndarray, ranks, a_off, b_off, h_in: int,
 
 def make_workload(name: str, seed: int | None = None, scale: str = "paper",
                   only_used: bool = False, idx: np.ndarray | None = None,
-                  n_adapters: int | None = None) -> Workload:
+                  n_adapters: int | None = None, h_out: int | None = None,
+                  stack_seed: int | None = None) -> Workload:
     """Build config ``name``.
 
     only_used: draw A/B only for adapters that ``idx`` references (the other
     adapters are zero); their bits match a full draw.
     idx / n_adapters: override the id draw or the adapter count (shapes stay).
+    h_out / stack_seed: another projection of the same layer: its own output
+    width and adapter stack (A/B drawn from stack_seed), with x, the ids, the
+    ranks and the scales of ``seed``.
     """
     c = CONFIGS[name]
+    if h_out is not None:
+        c = replace(c, h_out=h_out)
     if seed is None:
         seed = _CONFIG_SEED[name]
     N = c.N if n_adapters is None else n_adapters
@@ -230,17 +236,50 @@ def make_workload(name: str, seed: int | None = None, scale: str = "paper",
     A = np.zeros(int(a_sizes.sum()), np.uint16)
     B = np.zeros(int(b_sizes.sum()), np.uint16)
     ids = np.unique(idx[(idx >= 0) & (idx < N)]) if only_used else range(N)
-    fill_adapters(A, B, ranks, a_off, b_off, c.h_in, c.h_out, seed, scale, ids)
+    fill_adapters(A, B, ranks, a_off, b_off, c.h_in, c.h_out,
+                  seed if stack_seed is None else stack_seed, scale, ids)
     sx, _, _ = _stds(scale, c.h_in, int(ranks.max()) if N else 1)
     x = _normal_bits(_rng(seed, _TAG_X), (T, c.h_in), sx)
     if scale == "parity" or c.y_base == "zero":
         y_base = np.zeros((T, c.h_out), np.uint16)
     else:
-        y_base = _normal_bits(_rng(seed, _TAG_YB), (T, c.h_out), 1.0)
+        ys = seed if stack_seed is None else stack_seed
+        y_base = _normal_bits(_rng(ys, _TAG_YB), (T, c.h_out), 1.0)
     return Workload(name=name, T=T, n_adapters=N, h_in=c.h_in, h_out=c.h_out,
                     max_rank=int(ranks.max()) if N else 0, idx=idx, x=x,
                     y_base=y_base, ranks=ranks, a_off=a_off, b_off=b_off, A=A,
                     B=B, scales=scales, scale_kind=scale, seed=seed)
+
+
+# The LoRA-injected projections of one layer that read the same x, per
+# config: Llama-2-7B's attention projections q, k, v (4096 -> 4096 each,
+# section VII-A's 7B model) for the decode shape; for the prefill shape, the
+# GQA k and v projections (8192 -> 1024) and the q projection (8192 -> 8192).
+PROJECTIONS = {
+    "tiny": (256, 256, 128),
+    "decode": (4096, 4096, 4096),
+    "large": (4096, 4096, 4096),
+    "ragged": (5120, 5120, 5120),
+    "prefill": (8192, 1024, 1024),
+}
+
+
+def make_projections(name: str, n_proj: int | None = None, seed: int | None = None,
+                     scale: str = "paper", idx: np.ndarray | None = None,
+                     h_outs=None) -> list:
+    """Workloads of the projections of one layer sharing x and the ids: the
+    first is ``make_workload(name, ...)`` itself; projection p > 0 has its
+    own adapter stack (drawn from seed + 7919 p) and output width."""
+    if seed is None:
+        seed = _CONFIG_SEED[name]
+    hs = list(PROJECTIONS[name] if h_outs is None else h_outs)
+    if n_proj is not None:
+        hs = hs[:n_proj]
+    out = [make_workload(name, seed, scale, idx=idx, h_out=hs[0])]
+    for p in range(1, len(hs)):
+        out.append(make_workload(name, seed, scale, idx=out[0].idx, h_out=hs[p],
+                                 stack_seed=seed + 7919 * p))
+    return out
 
 
 def with_idx(w: Workload, idx: np.ndarray) -> Workload:

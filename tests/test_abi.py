@@ -25,7 +25,8 @@ def declared_functions():
 def test_header_declares_the_expected_calls():
     names = declared_functions()
     for fn in ("plora_segment", "plora_shrink", "plora_expand", "plora_apply",
-               "plora_workspace_bytes", "plora_status_string"):
+               "plora_apply_multi", "plora_workspace_bytes", "plora_workspace_bytes_multi",
+               "plora_status_string"):
         assert fn in names
     assert set(names) == set(P.EXPORTED)
 
@@ -209,3 +210,51 @@ def test_one_hip_runtime_per_process():
                          text=True, timeout=300)
     assert out.returncode == 0, out.stderr
     assert out.stdout.strip().splitlines()[-1] == "1"
+
+
+def _multi_status(ads, n=None, x=FAKE, ldx=256, ys=None, ldys=None, ws=FAKE, ws_bytes=None,
+                  seg=None):
+    seg = seg or _seg()
+    n = len(ads) if n is None else n
+    arr = (P.plora_adapters * max(len(ads), 1))(*ads)
+    ys = [FAKE] * len(ads) if ys is None else ys
+    ldys = [a.h_out for a in ads] if ldys is None else ldys
+    yarr = (ctypes.c_void_p * max(len(ys), 1))(*ys)
+    larr = (ctypes.c_int64 * max(len(ldys), 1))(*ldys)
+    if ws_bytes is None:
+        ws_bytes = P.lib.plora_workspace_bytes_multi(seg.T, arr, max(n, 1))
+    return P.lib.plora_apply_multi(x, ldx, arr, n, ctypes.byref(seg), yarr, larr, ws,
+                                   ws_bytes, None)
+
+
+def test_apply_multi_host_checks():
+    """plora_apply_multi's host-side rules, on fake device pointers (every
+    case returns before anything is launched)."""
+    a, b = _ad(), _ad(h_out=128)
+    # workspace: n cap8 tile slots, the largest partial-sum section
+    arr = (P.plora_adapters * 2)(a, b)
+    need = P.lib.plora_workspace_bytes_multi(8, arr, 2)
+    up = lambda v: (v + 255) // 256 * 256
+    slots = min(336, max(8, 2 * ((P.plora_tile_capacity(8, 4) + 7) // 8 * 8)))
+    assert need == up(up(up(336 * 8) + slots * 8 * 32 * 128 * 8) + 8 * 8 * 4)
+    assert need >= P.plora_workspace_bytes(8, a)
+    assert P.lib.plora_workspace_bytes_multi(8, arr, 0) == 0
+    assert P.lib.plora_workspace_bytes_multi(8, arr, P.PLORA_MAX_PROJECTIONS + 1) == 0
+    assert _multi_status([a, b], ws_bytes=need - 16) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
+    assert _multi_status([a, b], ws=None) == P.PLORA_ERR_INVALID_ARG
+    assert _multi_status([a, b], n=0) == P.PLORA_ERR_INVALID_ARG
+    assert _multi_status([a] * 9) == P.PLORA_ERR_UNSUPPORTED
+    # stacks must share n_adapters and h_in (one x, one batch)
+    assert _multi_status([a, _ad(h_in=512)]) == P.PLORA_ERR_INVALID_ARG
+    assert _multi_status([a, _ad(n_adapters=3)]) == P.PLORA_ERR_INVALID_ARG
+    # per-projection output checks
+    assert _multi_status([a, b], ys=[FAKE, None]) == P.PLORA_ERR_INVALID_ARG
+    assert _multi_status([a, b], ldys=[256, 64]) == P.PLORA_ERR_INVALID_ARG
+    assert _multi_status([a, b], ldys=[256, 132]) == P.PLORA_ERR_UNSUPPORTED
+    assert _multi_status([a, b], ys=[FAKE, FAKE + 8]) == P.PLORA_ERR_UNSUPPORTED
+    assert _multi_status([a, b], ldx=255) == P.PLORA_ERR_INVALID_ARG
+    # a bad stack is reported as for plora_apply
+    assert _multi_status([a, _ad(max_rank=12)]) == P.PLORA_ERR_UNSUPPORTED
+    # an empty batch launches nothing
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    assert _multi_status([a, b], seg=empty, ws=None, ws_bytes=0) == P.PLORA_OK

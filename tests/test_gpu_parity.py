@@ -494,3 +494,51 @@ def test_empty_and_all_skipped_batches(P):
     idx = np.full(w.T, -1, np.int32)
     y = Run(P, w, idx=idx).segment().apply()
     assert (y == w.y_base).all()
+
+
+# ---------------------------------------------------------------------------
+# several projections sharing x and the batch: plora_apply_multi
+# ---------------------------------------------------------------------------
+
+def _multi_run(P, ps, ws=None):
+    w0 = ps[0]
+    ads = [P.Adapters.from_workload(w) for w in ps]
+    segs = P.Segments(w0.T, w0.n_adapters)
+    P.segment(dev(w0.idx), segs)
+    ws = ws or P.Workspace(w0.T, ads)
+    x = dev(np.ascontiguousarray(w0.x).view(np.int16))
+    ys = [dev(np.ascontiguousarray(w.y_base).view(np.int16)) for w in ps]
+    P.apply_multi(x, ads, segs, ys, ws)
+    torch.cuda.synchronize()
+    return [bits16(y) for y in ys], (x, ads, segs, ws)
+
+
+@pytest.mark.parametrize("name,h_outs", [("tiny", None), ("decode", (4096, 1024, 4096)),
+                                         ("large", None), ("ragged", (5120, 1024)),
+                                         ("prefill", None)])
+def test_apply_multi_matches_oracle(P, name, h_outs):
+    ps = W.make_projections(name, scale="parity", h_outs=h_outs)
+    say(f"apply_multi {name} h_outs={[w.h_out for w in ps]} T={ps[0].T}")
+    ys, _ = _multi_run(P, ps)
+    stacks = [(w.A, w.a_off, w.B, w.b_off, w.ranks, w.scales, w.h_out) for w in ps]
+    outs = oracle.apply_multi(ps[0].x, ps[0].idx, stacks, [w.y_base for w in ps], ps[0].h_in,
+                              n_threads=ORACLE_THREADS)
+    for w, y, (yref, yout) in zip(ps, ys, outs):
+        check_y(y, yref, yout, w, strict_l2=True)
+
+
+def test_apply_multi_deterministic_and_like_separate_calls(P):
+    """Decode shape (one launch for all projections): bitwise repeatable; and
+    a batch too large for one launch runs plora_apply per projection, so its
+    bits equal separate calls."""
+    ps = W.make_projections("decode", scale="paper")
+    say("apply_multi determinism")
+    a, ctx = _multi_run(P, ps)
+    b, _ = _multi_run(P, ps, ws=ctx[3])
+    assert all((u == v).all() for u, v in zip(a, b))
+    ps = W.make_projections("prefill", scale="paper", h_outs=(1024, 512))
+    say("apply_multi per-projection path")
+    ys, _ = _multi_run(P, ps)
+    for w, y in zip(ps, ys):
+        single = Run(P, w).segment().apply()
+        assert (y == single).all()

@@ -473,3 +473,29 @@ def test_nan_and_inf_propagate():
     yref, _ = _apply(w, x=x)
     assert np.isnan(yref[0]).any() and not np.isfinite(yref[1]).all()
     assert np.isfinite(yref[2:]).all()
+
+
+def _stack(w):
+    return (w.A, w.a_off, w.B, w.b_off, w.ranks, w.scales, w.h_out)
+
+
+@pytest.mark.parametrize("name", ["tiny", "decode"])
+def test_apply_multi_each_projection_within_fp32_bound(name):
+    """Several projections sharing x and the ids (different stacks, output
+    widths): every projection's output lies within the fp32 bound of its own
+    float64 product, so no projection reads another's stack or width."""
+    ps = W.make_projections(name, scale="parity")
+    if name == "decode":
+        ps = [W.make_projections(name, scale="parity", h_outs=(4096, 1024, 512))[p]
+              for p in range(3)]
+    w0 = ps[0]
+    tokens = refs.sample_tokens(w0.T, 24)
+    outs = oracle.apply_multi(w0.x[tokens], w0.idx[tokens], [_stack(w) for w in ps],
+                              [w.y_base[tokens] for w in ps], w0.h_in)
+    assert len(outs) == len(ps)
+    for w, (yref, _) in zip(ps, outs):
+        assert yref.shape == (tokens.size, w.h_out)
+        y64, bound = refs.f64_reference(w, tokens)
+        assert (np.abs(yref.astype(np.float64) - y64) <= bound).all()
+    # the stacks really differ, and so do the outputs
+    assert not np.array_equal(outs[0][0][:, :ps[1].h_out], outs[1][0])
