@@ -107,15 +107,26 @@ typedef enum {
 #define PLORA_META_WORDS 8
 
 /*
- * The adapter stack.  Host struct; the pointers inside are device pointers.
+ * The adapter stack.  Host struct; the pointers inside are device pointers
+ * (the pools: device-accessible host memory).
  *   n_adapters  N, number of adapters (ids 0..N-1)
  *   h_in, h_out model dimensions D1, D2 (multiples of 8)
  *   max_rank    host upper bound on every ranks[i] (multiple of 8, <= 128);
  *               sizes the workspace and the v stride
- *   A, B        flat bf16 stacks of a_len and b_len elements
- *   a_off,b_off int64 [N] element offsets of A_i and B_i (multiples of 8)
+ *   A, B        flat bf16 stacks of a_len and b_len elements in device memory
+ *   a_off,b_off int64 [N] element offsets of A_i and B_i (multiples of 8);
+ *               an offset o < 0 names element -1 - o of the pool instead
  *   ranks       int32 [N], r_i in {0, 8, 16, 32, 64, 128}, r_i <= max_rank
  *   scales      fp32  [N], s_i
+ *   A_pool, B_pool, a_pool_len, b_pool_len
+ *               optional flat bf16 stacks in pinned host memory that the
+ *               kernels read directly, element counts (NULL / 0 if unused):
+ *               the pooled-memory placement of section V-A, where the GPU
+ *               loads A_i and B_i over the link itself (strategy E2); see
+ *               include/plora_placement.h for choosing what stays in device
+ *               memory.  A and B may be NULL when every offset is negative.
+ * Appended fields default to zero in C aggregate initialisation, so callers
+ * without pools need not set them.
  * Other ranks (the paper's range is 2..128 and its evaluation draws from
  * {8, 16, 32, 64, 128}) are stored zero-padded to the next of these sizes:
  * zero columns of A_i and zero rows of B_i leave every result unchanged.
@@ -133,6 +144,10 @@ typedef struct {
   const int64_t* b_off;
   const int32_t* ranks;
   const float* scales;
+  const uint16_t* A_pool;
+  const uint16_t* B_pool;
+  int64_t a_pool_len;
+  int64_t b_pool_len;
 } plora_adapters;
 
 /*
@@ -291,6 +306,12 @@ size_t plora_workspace_bytes_multi(int32_t T, const plora_adapters* ads, int32_t
  */
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
                                   hipStream_t stream);
+
+/* Host.  The device address of pinned host memory (hipHostMalloc'd, as
+ * torch's pin_memory gives), for the A_pool / B_pool fields; host is any
+ * address inside the allocation.  PLORA_ERR_UNSUPPORTED if the memory is not
+ * pinned and mapped for the device (kernels must never be handed it). */
+plora_status plora_pool_device_pointer(const void* host, const void** device);
 
 /* Static string naming a status code. */
 const char* plora_status_string(plora_status status);

@@ -513,6 +513,9 @@ struct ApplyArgs {
   const uint16_t* A;
   const uint16_t* B;
   int64_t a_len, b_len;
+  const uint16_t* A_pool;   // host-memory pools the device reads directly (may be null)
+  const uint16_t* B_pool;
+  int64_t a_pool_len, b_pool_len;
   const int64_t* a_off;
   const int64_t* b_off;
   const int32_t* ranks;
@@ -576,6 +579,20 @@ __device__ __forceinline__ Plan make_plan(const ApplyArgs& g, SliceKind kind) {
   return p;
 }
 
+// Start of an adapter's n-element block: offset o >= 0 is element o of the
+// device stack, o < 0 element -1 - o of the pool (host memory that the
+// device reads directly: the E2 analog, section V-A); null if the block is
+// misaligned or runs past its array.
+__device__ __forceinline__ const uint16_t* adapter_block(const uint16_t* dev, int64_t dev_len,
+                                                         const uint16_t* pool, int64_t pool_len,
+                                                         int64_t o, int64_t n) {
+  const bool in_pool = o < 0;
+  const int64_t e = in_pool ? -1 - o : o;
+  const uint16_t* base = in_pool ? pool : dev;
+  if (!base || (e & 7) || e + n > (in_pool ? pool_len : dev_len)) return nullptr;
+  return base + e;
+}
+
 // Read and validate tile u.  Returns false (for the whole work group) for
 // padding entries and for adapters the kernels must skip.  Threads below L
 // also fetch their tile row's token index (-1 if unusable); it is issued
@@ -593,10 +610,9 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
   if (my_tok < 0 || my_tok >= g.T) my_tok = -1;
   // ranks 8, 16, 32, 64, 128 (up to max_rank); anything else is skipped
   if (t.r < 8 || t.r > g.max_rank || (t.r & (t.r - 1))) return false;
-  if (ao < 0 || (ao & 7) || ao + (int64_t)g.h_in * t.r > g.a_len) return false;
-  if (bo < 0 || (bo & 7) || bo + (int64_t)g.h_out * t.r > g.b_len) return false;
-  t.Ai = g.A + ao;
-  t.Bi = g.B + bo;
+  t.Ai = adapter_block(g.A, g.a_len, g.A_pool, g.a_pool_len, ao, (int64_t)g.h_in * t.r);
+  t.Bi = adapter_block(g.B, g.b_len, g.B_pool, g.b_pool_len, bo, (int64_t)g.h_out * t.r);
+  if (!t.Ai || !t.Bi) return false;
   t.k0 = 0;
   t.k1 = g.h_in;
   t.j0 = 0;
@@ -1724,6 +1740,9 @@ struct ProjArgs {
   const uint16_t* A;
   const uint16_t* B;
   int64_t a_len, b_len;
+  const uint16_t* A_pool;
+  const uint16_t* B_pool;
+  int64_t a_pool_len, b_pool_len;
   const int64_t* a_off;
   const int64_t* b_off;
   const int32_t* ranks;
@@ -1753,6 +1772,8 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void apply_multi_kernel(MultiArgs m)
   ApplyArgs g = m.g;
   const ProjArgs& q = m.proj[p];
   g.A = q.A; g.B = q.B; g.a_len = q.a_len; g.b_len = q.b_len;
+  g.A_pool = q.A_pool; g.B_pool = q.B_pool; g.a_pool_len = q.a_pool_len;
+  g.b_pool_len = q.b_pool_len;
   g.a_off = q.a_off; g.b_off = q.b_off; g.ranks = q.ranks; g.scales = q.scales;
   g.y = q.y; g.ldy = q.ldy; g.h_out = q.h_out; g.max_rank = q.max_rank;
   apply_item(g, u, s, slot, stash, apply_lds);
@@ -1942,19 +1963,30 @@ size_t workspace_bytes(int32_t T, const plora_adapters* ad) { return ws_layout(T
 plora_status check_adapters_host(const plora_adapters* ad) {
   if (!ad) return PLORA_ERR_INVALID_ARG;
   if (ad->n_adapters < 0 || ad->h_in <= 0 || ad->h_out <= 0 || ad->max_rank < 0 ||
-      ad->a_len < 0 || ad->b_len < 0)
+      ad->a_len < 0 || ad->b_len < 0 || ad->a_pool_len < 0 || ad->b_pool_len < 0)
     return PLORA_ERR_INVALID_ARG;
   if ((ad->h_in & 7) || (ad->h_out & 7)) return PLORA_ERR_UNSUPPORTED;
   if (ad->max_rank == 0 || (ad->max_rank & 7) || ad->max_rank > PLORA_MAX_RANK)
     return PLORA_ERR_UNSUPPORTED;
   if (smem_bytes(ad->h_in, ad->max_rank) > kMaxLds) return PLORA_ERR_UNSUPPORTED;
   if (ad->n_adapters > 0 &&
-      (!ad->A || !ad->B || !ad->a_off || !ad->b_off || !ad->ranks || !ad->scales))
+      ((!ad->A && !ad->A_pool) || (!ad->B && !ad->B_pool) || !ad->a_off || !ad->b_off ||
+       !ad->ranks || !ad->scales))
     return PLORA_ERR_INVALID_ARG;
   if (!aligned16(ad->A) || !aligned16(ad->B) || !aligned16(ad->a_off) ||
-      !aligned16(ad->b_off) || !aligned16(ad->ranks) || !aligned16(ad->scales))
+      !aligned16(ad->b_off) || !aligned16(ad->ranks) || !aligned16(ad->scales) ||
+      !aligned16(ad->A_pool) || !aligned16(ad->B_pool))
     return PLORA_ERR_UNSUPPORTED;
   return PLORA_OK;
+}
+
+// Host mirror of adapter_block: whether offset o names an n-element block
+// inside the device stack (o >= 0) or the pool (o < 0).
+bool block_ok(const uint16_t* dev, int64_t dev_len, const uint16_t* pool, int64_t pool_len,
+              int64_t o, int64_t n) {
+  const bool in_pool = o < 0;
+  const int64_t e = in_pool ? -1 - o : o;
+  return (in_pool ? pool : dev) && (e & 7) == 0 && e + n <= (in_pool ? pool_len : dev_len);
 }
 
 plora_status check_segments_host(const plora_segments* seg, int32_t N) {
@@ -1992,6 +2024,8 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   if (st != PLORA_OK) return st;
   memset(&g, 0, sizeof g);
   g.A = ad->A; g.B = ad->B; g.a_len = ad->a_len; g.b_len = ad->b_len;
+  g.A_pool = ad->A_pool; g.B_pool = ad->B_pool;
+  g.a_pool_len = ad->a_pool_len; g.b_pool_len = ad->b_pool_len;
   g.a_off = ad->a_off; g.b_off = ad->b_off; g.ranks = ad->ranks; g.scales = ad->scales;
   g.perm = seg->perm;
   g.tiles = reinterpret_cast<const int4*>(seg->tiles);
@@ -2214,6 +2248,8 @@ plora_status plora_apply_multi(const uint16_t* x, int64_t ldx, const plora_adapt
   for (int p = 0; p < n_proj; ++p) {
     ProjArgs& q = m.proj[p];
     q.A = ads[p].A; q.B = ads[p].B; q.a_len = ads[p].a_len; q.b_len = ads[p].b_len;
+    q.A_pool = ads[p].A_pool; q.B_pool = ads[p].B_pool;
+    q.a_pool_len = ads[p].a_pool_len; q.b_pool_len = ads[p].b_pool_len;
     q.a_off = ads[p].a_off; q.b_off = ads[p].b_off; q.ranks = ads[p].ranks;
     q.scales = ads[p].scales; q.y = ys[p]; q.ldy = ldys[p]; q.h_out = ads[p].h_out;
     q.max_rank = ads[p].max_rank;
@@ -2250,8 +2286,10 @@ plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
       const int r = ranks[i];
       bool ok = usable_rank(r, ad->max_rank);
       if (ok && r > 0) {
-        ok = ao[i] >= 0 && (ao[i] & 7) == 0 && ao[i] + (int64_t)ad->h_in * r <= ad->a_len &&
-             bo[i] >= 0 && (bo[i] & 7) == 0 && bo[i] + (int64_t)ad->h_out * r <= ad->b_len;
+        ok = block_ok(ad->A, ad->a_len, ad->A_pool, ad->a_pool_len, ao[i],
+                      (int64_t)ad->h_in * r) &&
+             block_ok(ad->B, ad->b_len, ad->B_pool, ad->b_pool_len, bo[i],
+                      (int64_t)ad->h_out * r);
       }
       if (!ok) {
         if (bad_index) *bad_index = i;
@@ -2275,6 +2313,18 @@ const char* plora_status_string(plora_status status) {
     case PLORA_ERR_HIP: return "PLORA_ERR_HIP";
   }
   return "PLORA_ERR_UNKNOWN";
+}
+
+plora_status plora_pool_device_pointer(const void* host, const void** device) {
+  if (!host || !device) return PLORA_ERR_INVALID_ARG;
+  *device = nullptr;
+  void* d = nullptr;
+  if (hipHostGetDevicePointer(&d, const_cast<void*>(host), 0) != hipSuccess || !d) {
+    (void)hipGetLastError();
+    return PLORA_ERR_UNSUPPORTED;
+  }
+  *device = d;
+  return PLORA_OK;
 }
 
 int32_t plora_debug_last_hip_error(void) { return g_last_hip_error.load(); }

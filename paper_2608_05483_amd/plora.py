@@ -31,7 +31,8 @@ EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_ini
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
             "plora_apply_multi", "plora_workspace_bytes_multi",
             "plora_check_adapters", "plora_status_string",
-            "plora_debug_last_hip_error", "plora_debug_set_exchange_polls")
+            "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
+            "plora_pool_device_pointer")
 
 
 class PloraError(RuntimeError):
@@ -49,7 +50,9 @@ class plora_adapters(ctypes.Structure):
                 ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
                 ("a_len", ctypes.c_int64), ("b_len", ctypes.c_int64),
                 ("a_off", ctypes.c_void_p), ("b_off", ctypes.c_void_p),
-                ("ranks", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+                ("ranks", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("A_pool", ctypes.c_void_p), ("B_pool", ctypes.c_void_p),
+                ("a_pool_len", ctypes.c_int64), ("b_pool_len", ctypes.c_int64)]
 
 
 class plora_segments(ctypes.Structure):
@@ -91,6 +94,8 @@ def _load() -> ctypes.CDLL:
     L.plora_status_string.restype = ctypes.c_char_p
     L.plora_debug_last_hip_error.argtypes = []
     L.plora_debug_last_hip_error.restype = i32
+    L.plora_pool_device_pointer.argtypes = [P, ctypes.POINTER(P)]
+    L.plora_pool_device_pointer.restype = ctypes.c_int
     L.plora_debug_set_exchange_polls.argtypes = [i32]
     L.plora_debug_set_exchange_polls.restype = None
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
@@ -174,6 +179,12 @@ def plora_apply_multi(x: int, ldx: int, ads, seg: plora_segments, ys, ldys, ws: 
                                                    ws_bytes, stream))
 
 
+def plora_pool_device_pointer(host: int) -> int:
+    d = ctypes.c_void_p()
+    _ok("plora_pool_device_pointer", lib.plora_pool_device_pointer(host, ctypes.byref(d)))
+    return int(d.value)
+
+
 def plora_debug_set_exchange_polls(polls: int) -> None:
     lib.plora_debug_set_exchange_polls(polls)
 
@@ -200,15 +211,24 @@ class Adapters:
     """Device-resident adapter stack and its ABI struct."""
 
     def __init__(self, A, B, a_off, b_off, ranks, scales, h_in: int, h_out: int,
-                 max_rank: int):
+                 max_rank: int, A_pool=None, B_pool=None):
+        """A_pool / B_pool: optional pinned host tensors that negative offsets
+        name (element -1 - o)."""
         self.A, self.B = A, B
+        self.A_pool, self.B_pool = A_pool, B_pool
         self.a_off, self.b_off, self.ranks, self.scales = a_off, b_off, ranks, scales
         self.h_in, self.h_out, self.max_rank = h_in, h_out, max_rank
         self.n_adapters = int(ranks.numel())
+        ptr = lambda t: t.data_ptr() if t is not None else None
+        # pools: the device address of the pinned host memory (refused if the
+        # memory is not pinned and mapped)
+        pool = lambda t: plora_pool_device_pointer(t.data_ptr()) if t is not None else None
         self.struct = plora_adapters(
-            self.n_adapters, h_in, h_out, max_rank, A.data_ptr(), B.data_ptr(),
-            A.numel(), B.numel(), a_off.data_ptr(), b_off.data_ptr(),
-            ranks.data_ptr(), scales.data_ptr())
+            self.n_adapters, h_in, h_out, max_rank, ptr(A), ptr(B),
+            A.numel() if A is not None else 0, B.numel() if B is not None else 0,
+            a_off.data_ptr(), b_off.data_ptr(), ranks.data_ptr(), scales.data_ptr(),
+            pool(A_pool), pool(B_pool), A_pool.numel() if A_pool is not None else 0,
+            B_pool.numel() if B_pool is not None else 0)
 
     @classmethod
     def from_arrays(cls, A, B, a_off, b_off, ranks, scales, h_in, h_out,

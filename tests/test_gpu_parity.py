@@ -542,3 +542,49 @@ def test_apply_multi_deterministic_and_like_separate_calls(P):
     for w, y in zip(ps, ys):
         single = Run(P, w).segment().apply()
         assert (y == single).all()
+
+
+# ---------------------------------------------------------------------------
+# adapters read straight from pinned host memory (the pooled placement)
+# ---------------------------------------------------------------------------
+
+def test_adapters_read_from_a_pinned_host_pool(P):
+    """Odd adapters (then all of them) read from a pinned host pool through
+    negative offsets: the same kernels on the same values, so y is bit for bit
+    the all-device result, in both apply forms and in the split calls."""
+    for name in ("decode", "ragged"):
+        w = workload(name, "parity")
+        run = Run(P, w).segment()
+        y_dev = run.apply()
+        v_dev = run.shrink().cpu().numpy()
+        A_pool = torch.from_numpy(w.A.view(np.int16)).pin_memory()
+        B_pool = torch.from_numpy(w.B.view(np.int16)).pin_memory()
+        for pick in ("odd", "all"):
+            say(f"pool {name} {pick}")
+            sel = (np.arange(w.n_adapters) % 2 == 1) if pick == "odd" else \
+                np.ones(w.n_adapters, bool)
+            a_off = np.where(sel, -1 - w.a_off, w.a_off).astype(np.int64)
+            b_off = np.where(sel, -1 - w.b_off, w.b_off).astype(np.int64)
+            keep = pick == "odd"
+            ad = P.Adapters(run.ad.A if keep else None, run.ad.B if keep else None,
+                            dev(a_off), dev(b_off), run.ad.ranks, run.ad.scales, w.h_in,
+                            w.h_out, run.ad.max_rank, A_pool=A_pool, B_pool=B_pool)
+            assert P.plora_check_adapters(ad.struct, P._stream()) == -1
+            y = dev(run.y0.view(np.int16))
+            P.apply(run.x, ad, run.segs, y, run.ws)
+            v = torch.full((run.T, ad.max_rank), float("nan"), dtype=torch.float32,
+                           device="cuda")
+            P.shrink(run.x, ad, run.segs, v, run.ws)
+            torch.cuda.synchronize()
+            assert (bits16(y)[:, :w.h_out] == y_dev).all()
+            vv = v.cpu().numpy()
+            assert np.array_equal(np.isnan(vv), np.isnan(v_dev))
+            assert (vv[~np.isnan(vv)] == v_dev[~np.isnan(v_dev)]).all()
+
+
+def test_pool_pointer_must_be_pinned(P):
+    """Pageable host memory is refused before any kernel could touch it."""
+    t = torch.zeros(1024, dtype=torch.int16)
+    with pytest.raises(P.PloraError):
+        P.plora_pool_device_pointer(t.data_ptr())
+    assert P.plora_pool_device_pointer(t.pin_memory().data_ptr()) != 0
