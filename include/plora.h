@@ -58,7 +58,8 @@
  *                              pointer not 16-byte aligned; ldx/ldy not a
  *                              multiple of 8 or ldv not a multiple of 4;
  *                              T above PLORA_MAX_TOKENS; (N+1) * 2^ceil(log2 T)
- *                              beyond 2^32
+ *                              beyond 2^32; an adapter block of 2^31 bytes or
+ *                              more (max(h_in, h_out) * max_rank * 2)
  *   PLORA_ERR_WORKSPACE_TOO_SMALL  ws_bytes below plora_workspace_bytes()
  *                              where the call needs a workspace (a NULL ws
  *                              there is PLORA_ERR_INVALID_ARG)

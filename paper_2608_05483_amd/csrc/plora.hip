@@ -64,24 +64,42 @@ __device__ __forceinline__ uint4 ldg16(const uint16_t* p) {
 // place of the value there.  The load itself is unconditional: with a branch
 // around a load, the compiler waits for every load in flight where the
 // branches join instead of for the one it needs, and the vector path's
-// prefetching would be serialised.  Callers pick safe inside a line the same wavefront
-// reads anyway (the tile's first token row at the same column, the chunk
-// being loaded), so the masked lanes cost no extra traffic and no two work
-// groups pile onto one address.
+// prefetching would be serialised.  Used for activation rows (x, y), whose
+// lanes read different tokens' rows; callers pick safe inside a line the
+// same wavefront reads anyway (the tile's first token row), so masked lanes
+// cost no extra traffic.  Adapter blocks go through bld16 below instead.
 __device__ __forceinline__ uint4 ldg16z(const uint16_t* p, const uint16_t* safe, bool ok) {
   const uint4 v = ldg16(ok ? p : safe);
   return ok ? v : make_uint4(0, 0, 0, 0);
 }
 
-// The same with a branch around the load, for the matrix path: there, loads
-// are consumed chunk by chunk right after a barrier anyway, and the branch-free
-// form measured slower.
-__device__ __forceinline__ uint4 ldg16c(const uint16_t* p, bool ok) {
-  return ok ? ldg16(p) : make_uint4(0, 0, 0, 0);
+// The 8-byte form of ldg16z.
+__device__ __forceinline__ uint2 ldg8z(const uint16_t* p, const uint16_t* safe, bool ok) {
+  const uint2 v = *reinterpret_cast<const uint2*>(ok ? p : safe);
+  return ok ? v : make_uint2(0, 0);
 }
 
-__device__ __forceinline__ uint2 ldg8c(const uint16_t* p, bool ok) {
-  return ok ? *reinterpret_cast<const uint2*>(p) : make_uint2(0, 0);
+// An adapter block (A_i or B_i: n bf16 values at p) as a raw buffer
+// resource.  Loads through it are range-checked by the hardware: a lane
+// whose offset lies past the block reads zero and fetches nothing.  That
+// makes masked lanes free (no branch, so the compiler keeps its waits
+// exact, and no load of a stand-in address) and confines every read to
+// the block.  The host keeps blocks below 2^31 bytes (h_in and h_out times
+// max_rank), so kPastEnd lies past every one.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kRsrcWord3 = 0x00020000;   // raw buffer, 32-bit data format (gfx9 family)
+constexpr int kPastEnd = (int)0x80000000u;   // a byte offset past every block
+
+__device__ __forceinline__ Rsrc block_rsrc(const uint16_t* p, int64_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p), 0, (int)(n * 2),
+                                           kRsrcWord3);
+}
+
+// 16 bytes at element e of the block, zero where !ok.
+__device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
+  const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (int)(e * 2) : kPastEnd, 0, 0);
+  return make_uint4((uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w);
 }
 
 // ---------------------------------------------------------------------------
@@ -727,11 +745,11 @@ template <int BP>
 __device__ __forceinline__ void prefetch_b(const ApplyArgs& g, const Tile& t, uint4 (&bpre)[BP]) {
   const ExpandMap m = expand_map(t);
   const bool col_ok = m.co0 < m.n_oct;
-  const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + t.j0 + (int64_t)m.co0 * 8;
+  const Rsrc rb = block_rsrc(t.Bi, (int64_t)g.h_out * t.r);
+  const int64_t e0 = (int64_t)m.rb * g.h_out + t.j0 + (int64_t)m.co0 * 8;
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
 #pragma unroll
-  for (int j = 0; j < BP; ++j)
-    bpre[j] = ldg16z(bp + j * bstep, t.Bi + t.j0, col_ok && j < m.njb);
+  for (int j = 0; j < BP; ++j) bpre[j] = bld16(rb, e0 + j * bstep, col_ok && j < m.njb);
 }
 
 // This thread's y words (first column octet, row slot 0) of the tile's tokens.
@@ -841,6 +859,7 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
   uint16_t* xs = sm.buf;                   // [XW][TG]
   float* red = reinterpret_cast<float*>(sm.buf);  // [kW][TG][R], after xs is dead
 
+  const Rsrc ra = block_rsrc(t.Ai, (int64_t)g.h_in * t.r);
   float val[V];
 #pragma unroll
   for (int i = 0; i < V; ++i) val[i] = 0.f;
@@ -851,8 +870,7 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
     const int nj = tid < nq ? (nq - tid + kNT - 1) / kNT : 0;
     const int nj_max = (nq + kNT - 1) / kNT;       // the same for the whole group
     const int n8 = (w1 - w0) >> 3;                     // x chunks per token
-    const uint16_t* ap = t.Ai + ((int64_t)q0 + tid) * 8;
-    const uint16_t* a_safe = t.Ai + (int64_t)q0 * 8;
+    const int64_t ae = ((int64_t)q0 + tid) * 8;       // this thread's first chunk
     const uint16_t* x_safe = g.x + (int64_t)max(sm.tok[0], 0) * g.ldx + w0;
     uint4 xr[XR], apre[AP];
 #pragma unroll
@@ -864,7 +882,7 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
     }
 #pragma unroll
     for (int j = 0; j < AP; ++j)
-      apre[j] = ldg16z(ap + (int64_t)j * kNT * 8, a_safe, j < nj);
+      apre[j] = bld16(ra, ae + (int64_t)j * kNT * 8, j < nj);
     if (prefetch && w0 == t.k0) {
       prefetch_b<bp_depth<TG>()>(g, t, bpre);
       prefetch_y<TG>(g, t, sm.tok, ypre);
@@ -888,19 +906,18 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
     uint4 a0[kCH], a1[kCH];
 #pragma unroll
     for (int j = 0; j < kCH; ++j)
-      a0[j] = ldg16z(ap + (int64_t)(AP + j) * kNT * 8, a_safe, AP + j < nj);
+      a0[j] = bld16(ra, ae + (int64_t)(AP + j) * kNT * 8, AP + j < nj);
 #pragma unroll
     for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
     if (nj_max > AP) {
       for (int jb = AP; jb < nj_max; jb += 2 * kCH) {
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          a1[j] = ldg16z(ap + (int64_t)(jb + kCH + j) * kNT * 8, a_safe, jb + kCH + j < nj);
+          a1[j] = bld16(ra, ae + (int64_t)(jb + kCH + j) * kNT * 8, jb + kCH + j < nj);
         fma_a<R_OCT, TG>(val, a0, xs, q0, w0, jb, nj);
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          a0[j] = ldg16z(ap + (int64_t)(jb + 2 * kCH + j) * kNT * 8, a_safe,
-                         jb + 2 * kCH + j < nj);
+          a0[j] = bld16(ra, ae + (int64_t)(jb + 2 * kCH + j) * kNT * 8, jb + 2 * kCH + j < nj);
         fma_a<R_OCT, TG>(val, a1, xs, q0, w0, jb + kCH, nj);
       }
     }
@@ -975,11 +992,12 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
   constexpr int BP = bp_depth<TG>();
   const ExpandMap m = expand_map(t);
   const int n_oct = m.n_oct;
+  const Rsrc rb = block_rsrc(t.Bi, (int64_t)g.h_out * t.r);
   const int64_t bstep = (int64_t)m.RSB * g.h_out;
   for (int cb = 0, co = m.co0; cb * kW * m.CPW < n_oct; ++cb, co += kW * m.CPW) {
     const bool col_ok = co < n_oct;
     const int jc = t.j0 + co * 8;                    // first y column of the octet
-    const uint16_t* bp = t.Bi + (int64_t)m.rb * g.h_out + jc;
+    const int64_t be = (int64_t)m.rb * g.h_out + jc;   // this thread's first B_i unit
     float d[TG * 8];
 #pragma unroll
     for (int i = 0; i < TG * 8; ++i) d[i] = 0.f;
@@ -994,7 +1012,7 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
         uint4 b[kCH];
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          b[j] = ldg16z(bp + (int64_t)(jb + j) * bstep, t.Bi + jc, jb + j < m.njb);
+          b[j] = bld16(rb, be + (int64_t)(jb + j) * bstep, jb + j < m.njb);
         fma_b<TG>(d, b, sm, m, jb);
       }
     }
@@ -1012,22 +1030,25 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
                  : ldg16z(g.y + (int64_t)tk * g.ldy + jc,
                           g.y + (int64_t)max(sm.tok[0], 0) * g.ldy + jc, tk >= 0);
       }
+      // every token's words first, then the stores (as in the matrix path:
+      // a y word used after a store would make the compiler wait for it)
+      uint4 out[TG];
+#pragma unroll
+      for (int tt = 0; tt < TG; ++tt) {
+        float yf[8];
+        unpack8(yv[tt], yf);
+        uint32_t ob[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[tt * 8 + e], yf[e]));
+        out[tt].x = ob[0] | (ob[1] << 16);
+        out[tt].y = ob[2] | (ob[3] << 16);
+        out[tt].z = ob[4] | (ob[5] << 16);
+        out[tt].w = ob[6] | (ob[7] << 16);
+      }
 #pragma unroll
       for (int tt = 0; tt < TG; ++tt) {
         const int tk = tt < t.L ? sm.tok[tt] : -1;
-        if (tk >= 0) {
-          float yf[8];
-          unpack8(yv[tt], yf);
-          uint32_t ob[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) ob[e] = to_bf16(fmaf(t.s, d[tt * 8 + e], yf[e]));
-          uint4 out;
-          out.x = ob[0] | (ob[1] << 16);
-          out.y = ob[2] | (ob[3] << 16);
-          out.z = ob[4] | (ob[5] << 16);
-          out.w = ob[6] | (ob[7] << 16);
-          *reinterpret_cast<uint4*>(g.y + (int64_t)tk * g.ldy + jc) = out;
-        }
+        if (tk >= 0) *reinterpret_cast<uint4*>(g.y + (int64_t)tk * g.ldy + jc) = out[tt];
       }
     }
   }
@@ -1078,6 +1099,30 @@ __device__ __forceinline__ uint64_t xload(const uint64_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Exchange words are written and polled at agent scope (`sc1` on gfx950):
+// stores reach memory and polls read past the compute unit's L1 and the
+// XCD's L2, so a partner's word is seen wherever the partner ran.  (At
+// work-group scope, `sc0`, most partners' words were never seen, even with
+// a tile's items on one XCD and the L1 invalidated before each poll.)
+__device__ __forceinline__ uint64_t xpoll(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void xpublish(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Item b of an exchange-form launch with S slices per tile slot: slice s
+// of slot q, b = q S + s.  A slot's items are neighbours in the grid, so
+// they are dispatched together, and (work group b runs on XCD b mod 8) they
+// spread over the XCDs.  Numbering a slot's items onto one XCD instead
+// measured 1.5 us slower per decode-shaped call: the exchange goes through
+// memory either way, and the spread balances the XCDs.
+__device__ __forceinline__ void exchange_item(int b, int S, int& q, int& s) {
+  q = b / S;
+  s = b - q * S;
+}
+
 // Publish this item's partial v (sm.vs) and replace sm.vs by the sum of all
 // S partials, in slice order (the order plora_shrink and the two-launch form
 // sum them in).  Entry o = l r + c of the tile keeps its kMaxSlices words
@@ -1090,9 +1135,7 @@ __device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const 
   const uint64_t tagw = (uint64_t)xc.tag << 32;
   for (int o = threadIdx.x; o < n; o += kNT) {
     const int l = o / t.r, c = o - l * t.r;
-    __hip_atomic_store(xc.words + o * kMaxSlices + xc.s,
-                       tagw | __float_as_uint(sm.vs[c * kTT + l]), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+    xpublish(xc.words + o * kMaxSlices + xc.s, tagw | __float_as_uint(sm.vs[c * kTT + l]));
   }
   bool late = false;
   for (int o = threadIdx.x; o < n; o += kNT) {
@@ -1102,7 +1145,7 @@ __device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const 
     for (int it = 0; !ready && it <= xc.polls; ++it) {
       if (it > 0) __builtin_amdgcn_s_sleep(2);
 #pragma unroll
-      for (int q = 0; q < kMaxSlices; ++q) w[q] = xload(e + q);
+      for (int q = 0; q < kMaxSlices; ++q) w[q] = xpoll(e + q);
       ready = true;
 #pragma unroll
       for (int q = 0; q < kMaxSlices; ++q)
@@ -1119,10 +1162,11 @@ __device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const 
   return __syncthreads_or(late) == 0;
 }
 
-// An expand-only call with a hook (the one-launch form's exchange of v)
-// requests its first chunks of B_i and its y words, then runs the hook,
-// which leaves the final v in sm.vs, then expands: the loads travel while
-// the hook waits.
+// A tile's pass: shrink (v of rows [k0, k1) into sm.vs), expand (columns
+// [j0, j1) from sm.vs), or both; with both, the expand's first loads of
+// B_i and y are requested with the shrink's.  The hook runs between the
+// two (the one-launch form's exchange, which turns the partial v into the
+// full one) while those loads travel; only a pass with both takes one.
 struct NoHook {
   __device__ void operator()() const {}
 };
@@ -1134,7 +1178,7 @@ __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, 
   uint4 bpre[bp_depth<TG>()], ypre[TG];
 #pragma unroll
   for (int i = 0; i < TG; ++i) ypre[i] = make_uint4(0, 0, 0, 0);
-  bool have_y = do_shrink;
+  const bool have_y = do_shrink;
   if (do_shrink) {
     switch (t.r >> 3) {
       case 1: shrink_valu<1, TG>(g, t, sm, bpre, ypre, do_expand); break;
@@ -1143,13 +1187,9 @@ __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, 
       case 8: shrink_valu<8, TG>(g, t, sm, bpre, ypre, do_expand); break;
       default: shrink_valu<16, TG>(g, t, sm, bpre, ypre, do_expand); break;
     }
+    if (hooked) hook();
   } else {
     prefetch_b<bp_depth<TG>()>(g, t, bpre);
-    if (hooked) {
-      prefetch_y<TG>(g, t, sm.tok, ypre);
-      hook();
-      have_y = true;
-    }
   }
   if (do_expand) expand_valu<TG>(g, t, sm, bpre, ypre, have_y);
 }
@@ -1400,40 +1440,100 @@ __device__ __forceinline__ void split_v(const Tile& t, const Smem& sm, int RK) {
   }
 }
 
-// Expand of a multi-token tile with MT token tiles of 16: D^T[j][token] =
-// sum_c B_i[c][j] (vhi + vlo)[token][c], then y = bf16(y + s D).
-template <int MT, class H>
-__device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                            H&& hook) {
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4;
-  const int r = t.r;
-  const int RK = rk_max(g.max_rank);
-  const int rk = r < kRK ? kRK : r;                // K extent, zero rows above r
-  const int JC = min(kChunk / rk, (t.j1 - t.j0 + 15) / 16 * 16);   // columns per chunk
-  const int nchunks = (t.j1 - t.j0 + JC - 1) / JC;
-  uint16_t* Bs = sm.buf;
-  const uint16_t* vhi = sm.vhl;
-  const uint16_t* vlo = sm.vhl + kTT * RK;
-  constexpr int JT = 8;                            // j tiles per wave per chunk (max)
+// The matrix-path expand streams B_i in column chunks of JC columns (as
+// many as fit kChunk elements at K extent rk = max(r, kRK)), with each
+// wavefront's y words of a chunk in registers.  ExpandPre holds this
+// thread's share of one chunk: its B_i units (before they go to LDS) and
+// the y words of its j tiles.
+constexpr int kJT = 8;                             // j tiles per wave per chunk (max)
+
+template <int MT>
+struct ExpandPre {
   uint4 breg[8];
-  uint2 yv[JT][MT];
-  int toks[MT];
+  uint2 yv[kJT][MT];
+};
+
+__device__ __forceinline__ int expand_chunk_cols(const Tile& t) {
+  const int rk = t.r < kRK ? kRK : t.r;
+  return min(kChunk / rk, (t.j1 - t.j0 + 15) / 16 * 16);
+}
+
+// Token of this lane's tile row in token tile nt (-1 past the tile).
+template <int MT>
+__device__ __forceinline__ void expand_toks(const Tile& t, const Smem& sm, int (&toks)[MT]) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int nt = 0; nt < MT; ++nt) {
     const int ti = nt * 16 + (lane & 15);
     toks[nt] = ti < t.L ? sm.tok[ti] : -1;
   }
-  auto load_b = [&](int j0) {
-    const int cols = min(JC, t.j1 - j0);
-    const int per_row = cols >> 3;
-    const int n16 = r * per_row;
+}
+
+// This thread's B_i units of the chunk starting at column j0.
+template <int MT>
+__device__ __forceinline__ void expand_load_b(const ApplyArgs& g, const Tile& t, int j0, int JC,
+                                              ExpandPre<MT>& pre) {
+  const int cols = min(JC, t.j1 - j0);
+  const int per_row = cols >> 3;
+  const int n16 = t.r * per_row;
+  const Rsrc rb = block_rsrc(t.Bi, (int64_t)g.h_out * t.r);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int q = tid + j * kNT;
-      const int c = q / per_row, col = q - c * per_row;
-      breg[j] = ldg16c(t.Bi + (int64_t)c * g.h_out + j0 + col * 8, q < n16);
-    }
-  };
+  for (int j = 0; j < 8; ++j) {
+    const int q = (int)threadIdx.x + j * kNT;
+    const int c = q / per_row, col = q - c * per_row;
+    pre.breg[j] = bld16(rb, (int64_t)c * g.h_out + j0 + col * 8, q < n16);
+  }
+}
+
+// y words of this wave's j tiles of the chunk starting at column j0.
+template <int MT>
+__device__ __forceinline__ void expand_load_y(const ApplyArgs& g, const Tile& t, int j0, int JC,
+                                              const int (&toks)[MT], ExpandPre<MT>& pre) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, grp = lane >> 4;
+  const int njt = (min(JC, t.j1 - j0) + 15) / 16;
+  // masked lanes read the tile's first token row at the chunk's first column
+  const int tok0 = __builtin_amdgcn_readfirstlane(toks[0]);   // lane 0: tile row 0
+  const uint16_t* y_safe = g.y + (int64_t)max(tok0, 0) * g.ldy + j0;
+#pragma unroll
+  for (int i = 0; i < kJT; ++i) {
+    const int jt = w + i * kW;
+    const int j = j0 + jt * 16 + 4 * grp;
+    const bool jok = jt < njt && j < t.j1;
+#pragma unroll
+    for (int nt = 0; nt < MT; ++nt)
+      pre.yv[i][nt] = ldg8z(g.y + (int64_t)toks[nt] * g.ldy + j, y_safe, jok && toks[nt] >= 0);
+  }
+}
+
+// The first chunk's B_i units and y words, requested ahead of the expand.
+template <int MT>
+__device__ __forceinline__ void expand_prefetch(const ApplyArgs& g, const Tile& t,
+                                                const Smem& sm, ExpandPre<MT>& pre) {
+  int toks[MT];
+  expand_toks<MT>(t, sm, toks);
+  const int JC = expand_chunk_cols(t);
+  expand_load_b<MT>(g, t, t.j0, JC, pre);
+  expand_load_y<MT>(g, t, t.j0, JC, toks, pre);
+}
+
+// Expand of a multi-token tile with MT token tiles of 16: D^T[j][token] =
+// sum_c B_i[c][j] (vhi + vlo)[token][c], then y = bf16(y + s D).  Unless
+// `fetched` (expand_prefetch already requested them), the first chunk's
+// B_i and y are requested here, before the hook runs.
+template <int MT, class H>
+__device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                            H&& hook, ExpandPre<MT>& pre, bool fetched) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, grp = lane >> 4;
+  const int r = t.r;
+  const int RK = rk_max(g.max_rank);
+  const int rk = r < kRK ? kRK : r;                // K extent, zero rows above r
+  const int JC = expand_chunk_cols(t);             // columns per chunk
+  const int nchunks = (t.j1 - t.j0 + JC - 1) / JC;
+  uint16_t* Bs = sm.buf;
+  const uint16_t* vhi = sm.vhl;
+  const uint16_t* vlo = sm.vhl + kTT * RK;
+  int toks[MT];
+  expand_toks<MT>(t, sm, toks);
   auto store_b = [&](int j0) {
     const int cols = min(JC, t.j1 - j0);
     const int per_row = cols >> 3;
@@ -1444,7 +1544,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       const int q = tid + j * kNT;
       if (q < n16) {
         const int c = q / per_row, col = q - c * per_row;
-        *reinterpret_cast<uint4*>(Bs + c * S + col * 8) = breg[j];
+        *reinterpret_cast<uint4*>(Bs + c * S + col * 8) = pre.breg[j];
       }
     }
     // zero padding: columns [cols, S) of rows < r, and rows [r, rk)
@@ -1455,23 +1555,10 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
       *reinterpret_cast<uint4*>(Bs + r * S + q * 8) = make_uint4(0, 0, 0, 0);
   };
 
-  // y words of this wave's j tiles of the chunk starting at column j0
-  auto load_y = [&](int j0) {
-    const int njt = (min(JC, t.j1 - j0) + 15) / 16;
-#pragma unroll
-    for (int i = 0; i < JT; ++i) {
-      const int jt = w + i * kW;
-      const int j = j0 + jt * 16 + 4 * grp;
-      const bool jok = jt < njt && j < t.j1;
-#pragma unroll
-      for (int nt = 0; nt < MT; ++nt)
-        yv[i][nt] = ldg8c(g.y + (int64_t)toks[nt] * g.ldy + j, jok && toks[nt] >= 0);
-    }
-  };
-
-  // the first chunk's B_i and y are requested before the hook runs
-  load_b(t.j0);
-  load_y(t.j0);
+  if (!fetched) {
+    expand_load_b<MT>(g, t, t.j0, JC, pre);
+    expand_load_y<MT>(g, t, t.j0, JC, toks, pre);
+  }
   hook();
   for (int ch = 0; ch < nchunks; ++ch) {
     const int j0 = t.j0 + ch * JC;
@@ -1481,11 +1568,18 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     store_b(j0);
     lds_sync();
     // y words of this chunk (the first came before), then the next chunk of B_i
-    if (ch > 0) load_y(j0);
-    if (ch + 1 < nchunks) load_b(j0 + JC);
+    if (ch > 0) expand_load_y<MT>(g, t, j0, JC, toks, pre);
+    if (ch + 1 < nchunks) expand_load_b<MT>(g, t, j0 + JC, JC, pre);
+    // every j tile's output words first, then every store: a use of a y
+    // word after a store makes the compiler wait for that store too (the
+    // guards hide the exact count from it), which serialised one store
+    // round trip per j tile
+    uint2 out[kJT][MT];
 #pragma unroll
-    for (int i = 0; i < JT; ++i) {
+    for (int i = 0; i < kJT; ++i) {
       const int jt = w + i * kW;
+#pragma unroll
+      for (int nt = 0; nt < MT; ++nt) out[i][nt] = make_uint2(0, 0);
       if (jt < njt) {
         f32x4_t acc[MT];
 #pragma unroll
@@ -1501,21 +1595,26 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
             acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_bf16x8(lo), acc[nt], 0, 0, 0);
           }
         }
-        const int j = j0 + jt * 16 + 4 * grp;
 #pragma unroll
         for (int nt = 0; nt < MT; ++nt) {
-          if (toks[nt] >= 0 && j < t.j1) {
-            const uint2 yw = yv[i][nt];
-            const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
-            const uint32_t o0 = to_bf16(fmaf(t.s, acc[nt][0], y0));
-            const uint32_t o1 = to_bf16(fmaf(t.s, acc[nt][1], y1));
-            const uint32_t o2 = to_bf16(fmaf(t.s, acc[nt][2], y2));
-            const uint32_t o3 = to_bf16(fmaf(t.s, acc[nt][3], y3));
-            *reinterpret_cast<uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j) =
-                make_uint2(o0 | (o1 << 16), o2 | (o3 << 16));
-          }
+          const uint2 yw = pre.yv[i][nt];
+          const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
+          const uint32_t o0 = to_bf16(fmaf(t.s, acc[nt][0], y0));
+          const uint32_t o1 = to_bf16(fmaf(t.s, acc[nt][1], y1));
+          const uint32_t o2 = to_bf16(fmaf(t.s, acc[nt][2], y2));
+          const uint32_t o3 = to_bf16(fmaf(t.s, acc[nt][3], y3));
+          out[i][nt] = make_uint2(o0 | (o1 << 16), o2 | (o3 << 16));
         }
       }
+    }
+#pragma unroll
+    for (int i = 0; i < kJT; ++i) {
+      const int jt = w + i * kW;
+      const int j = j0 + jt * 16 + 4 * grp;
+#pragma unroll
+      for (int nt = 0; nt < MT; ++nt)
+        if (jt < njt && toks[nt] >= 0 && j < t.j1)
+          *reinterpret_cast<uint2*>(g.y + (int64_t)toks[nt] * g.ldy + j) = out[i][nt];
     }
     lds_sync();
   }
@@ -1541,21 +1640,28 @@ __device__ __forceinline__ void shrink_mfma_r(const ApplyArgs& g, const Tile& t,
   }
 }
 
-template <class H>
-__device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
-                                          bool do_shrink, bool do_expand, bool hooked, H&& hook) {
+template <int MT, class H>
+__device__ __forceinline__ void mfma_tile_mt(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                             bool do_shrink, bool do_expand, bool hooked,
+                                             H&& hook) {
   const int RK = rk_max(g.max_rank);
+  ExpandPre<MT> pre;
+  // with both halves and the hook between them (the exchange form, whose
+  // items read small slices), the expand's first B_i and y loads leave
+  // ahead of the shrink's, so they travel while it runs (tiles of up to 16
+  // tokens: with two token tiles the registers they take would spill)
+  const bool early = MT == 1 && do_shrink && do_expand && hooked;
+  if (early) expand_prefetch<MT>(g, t, sm, pre);
   // v's bf16 split is read for every token row < 16 * MT and column < K extent
   for (int o = threadIdx.x; o < 2 * kTT * RK; o += kNT) sm.vhl[o] = 0;
   lds_sync();
-  const bool two = t.L > 16;
   if (do_shrink) {
     shrink_mfma_r(g, t, sm);
-  } else if (!hooked) {
+  } else {
     split_v(t, sm, RK);
     lds_sync();
   }
-  // with a hook, v is final only after it has run: split it then
+  // with a hook, v is final only after it has run: split it again then
   auto after_b = [&] {
     if (hooked) {
       hook();
@@ -1563,10 +1669,14 @@ __device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, con
       lds_sync();
     }
   };
-  if (do_expand) {
-    if (two) expand_mfma<2>(g, t, sm, after_b);
-    else expand_mfma<1>(g, t, sm, after_b);
-  }
+  if (do_expand) expand_mfma<MT>(g, t, sm, after_b, pre, early);
+}
+
+template <class H>
+__device__ __forceinline__ void mfma_tile(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                          bool do_shrink, bool do_expand, bool hooked, H&& hook) {
+  if (t.L > 16) mfma_tile_mt<2>(g, t, sm, do_shrink, do_expand, hooked, hook);
+  else mfma_tile_mt<1>(g, t, sm, do_shrink, do_expand, hooked, hook);
 }
 
 __device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
@@ -1576,12 +1686,15 @@ __device__ __forceinline__ void tile_dispatch(const ApplyArgs& g, const Tile& t,
   else valu_tile(g, t, sm, do_shrink, do_expand, false, NoHook{});
 }
 
-// Expand only, with hook() run once the first loads of B_i are on their way.
+// Shrink of the tile's rows [k0, k1), hook(), then expand of its columns
+// [j0, j1): the expand's first loads of B_i and y are requested with the
+// shrink's, and the hook (the exchange that turns the partial v into the
+// full one) runs while they travel.
 template <class H>
-__device__ __forceinline__ void expand_hooked(const ApplyArgs& g, const Tile& t, const Smem& sm,
+__device__ __forceinline__ void tile_exchange(const ApplyArgs& g, const Tile& t, const Smem& sm,
                                               H&& hook) {
-  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, false, true, true, hook);
-  else valu_tile(g, t, sm, false, true, true, hook);
+  if (t.L > vector_tokens(t.r)) mfma_tile(g, t, sm, true, true, true, hook);
+  else valu_tile(g, t, sm, true, true, true, hook);
 }
 
 // Common prologue: token indices to LDS, v zeroed.
@@ -1676,8 +1789,8 @@ __device__ __forceinline__ void plain_v(const ApplyArgs& g, const Tile& t, const
 // tile: slice s of tile u, exchanging through tile slot `slot` (its region
 // and epoch in the workspace): the shrink of h_in rows [s KR, (s+1) KR),
 // the exchange of partial v with the tile's other items, and the expand of
-// y columns [s W, (s+1) W), whose first loads of B_i and y are issued before
-// the exchange waits.  If the exchange times out, plain_v computes v here.
+// y columns [s W, (s+1) W), whose first loads of B_i and y are issued with
+// the shrink's.  If the exchange times out, plain_v computes v here.
 __device__ __forceinline__ void apply_item(const ApplyArgs& g, int u, int s, int slot,
                                            ItemStash& stash, unsigned char* lds) {
   {
@@ -1696,25 +1809,17 @@ __device__ __forceinline__ void apply_item(const ApplyArgs& g, int u, int s, int
   const Smem sm = carve(lds, g.max_rank);
   const int S = g.fixed_slices;
   const int KR = ((g.h_in + S - 1) / S + 63) & ~63;
-  {
-    Tile t = unstash(&stash);
-    t.k0 = uni(stash.slice) * KR;
-    t.k1 = min(g.h_in, t.k0 + KR);
-    t.j0 = 0;
-    t.j1 = g.h_out;
-    tile_dispatch(g, t, sm, true, false);
-  }
+  const int W = ((g.h_out + S - 1) / S + 15) & ~15;
   {
     Tile t = unstash(&stash);
     const int sl = uni(stash.slice);
-    const int W = ((g.h_out + S - 1) / S + 15) & ~15;
-    t.k0 = 0;
-    t.k1 = g.h_in;
+    t.k0 = sl * KR;
+    t.k1 = min(g.h_in, t.k0 + KR);
     t.j0 = sl * W;
     t.j1 = min(g.h_out, t.j0 + W);
     const Xchg xc{sl, S, KR, (uint32_t)(stash.ep + 1),
                   g.xw + (int64_t)uni(stash.u) * kSlotWords, g.polls};
-    expand_hooked(g, t, sm, [&] {
+    tile_exchange(g, t, sm, [&] {
       if (!exchange_v(t, sm, xc)) plain_v(g, t, sm);
     });
   }
@@ -1723,15 +1828,15 @@ __device__ __forceinline__ void apply_item(const ApplyArgs& g, int u, int s, int
                            __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// plora_apply as one launch, tiles in S > 1 slices: item blockIdx.x = u S + s
-// (S chosen on the host, so the item needs no count from the device), tile
-// slot u.  A tile's items are neighbours in the grid, so the work groups a
-// tile waits on are dispatched with it.
+// plora_apply as one launch, tiles in S > 1 slices (S chosen on the host, so
+// the item needs no count from the device): work group blockIdx.x is slice
+// s of tile u, tile slot u, as exchange_item numbers them, so the work
+// groups a tile waits on are dispatched with it.
 __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   __shared__ ItemStash stash;
-  const int S = g.fixed_slices;
-  const int u = (int)blockIdx.x / S, s = (int)blockIdx.x - u * S;
+  int u, s;
+  exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   apply_item(g, u, s, u, stash, apply_lds);
 }
 
@@ -1759,14 +1864,14 @@ struct MultiArgs {
   int32_t cap8;           // tile capacity rounded up to 8
 };
 
-// Several projections in one launch, S > 1 slices per tile: item
-// blockIdx.x = (p cap8 + u) S + s is slice s of tile u of projection p,
-// exchanging through tile slot p cap8 + u.
+// Several projections in one launch, S > 1 slices per tile: tile slot
+// p cap8 + u (numbered as exchange_item numbers slots) is tile u of
+// projection p, and exchanges through that slot.
 __global__ __launch_bounds__(kNT, kWGPerCU) void apply_multi_kernel(MultiArgs m) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   __shared__ ItemStash stash;
-  const int S = m.g.fixed_slices;
-  const int slot = (int)blockIdx.x / S, s = (int)blockIdx.x - slot * S;
+  int slot, s;
+  exchange_item((int)blockIdx.x, m.g.fixed_slices, slot, s);
   const int p = slot / m.cap8, u = slot - p * m.cap8;
   if (p >= m.n_proj) return;
   ApplyArgs g = m.g;
@@ -1966,6 +2071,9 @@ plora_status check_adapters_host(const plora_adapters* ad) {
       ad->a_len < 0 || ad->b_len < 0 || ad->a_pool_len < 0 || ad->b_pool_len < 0)
     return PLORA_ERR_INVALID_ARG;
   if ((ad->h_in & 7) || (ad->h_out & 7)) return PLORA_ERR_UNSUPPORTED;
+  // adapter blocks are read through 32-bit byte offsets
+  if ((int64_t)std::max(ad->h_in, ad->h_out) * std::max(ad->max_rank, 0) * 2 >= (INT64_C(1) << 31))
+    return PLORA_ERR_UNSUPPORTED;
   if (ad->max_rank == 0 || (ad->max_rank & 7) || ad->max_rank > PLORA_MAX_RANK)
     return PLORA_ERR_UNSUPPORTED;
   if (smem_bytes(ad->h_in, ad->max_rank) > kMaxLds) return PLORA_ERR_UNSUPPORTED;
