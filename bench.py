@@ -2,23 +2,27 @@
 """Benchmark: the batched heterogeneous-adapter LoRA apply on one MI355X.
 
 One step = one pass of the whole hot path over one batch already resident in
-HBM: plora_segment (group the batch's tokens by adapter) then plora_apply
-(y += s_i (x A_i) B_i for every token).  Each step takes a fresh
-token-to-adapter draw from a pool drawn up front, and a different replica of
-the adapter stack, so that an adapter's bytes are never still sitting in the
-256 MB Infinity Cache from an earlier step (a served model revisits one
-projection's stack only after every other LoRA projection of every layer).
+HBM: plora_segment_apply, which groups the batch's tokens by adapter (the
+plora_segment outputs) and applies y += s_i (x A_i) B_i for every token.  For
+decode-sized batches that is one launch; larger batches take plora_segment
+then plora_apply.  With --projections > 1 a step is plora_segment then one
+plora_apply_multi.  Each step takes a fresh token-to-adapter draw from a pool
+drawn up front, and a different replica of the adapter stack, so that an
+adapter's bytes are never still sitting in the 256 MB Infinity Cache from an
+earlier step (a served model revisits one projection's stack only after every
+other LoRA projection of every layer).
 
 Prints ONE JSON line.  ``value`` is whole-job tokens/s over the timed steps
-(wall clock, segment + apply), the K steps launched as one captured HIP graph
-(``--eager``: one launch per kernel from Python; the eager time is reported
-too).  ``roofline`` prices the dominant kernel,
-plora_apply: algorithmic bytes per call (distinct adapters' A_i and B_i,
-2 r_i (h_in + h_out) bytes each, plus x read, y read and written, and the
-token permutation) over its average duration: K calls captured as one HIP
-graph and replayed between two HIP events recorded on the stream the
-kernels run on.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
-the same workload.
+(wall clock), the K steps launched as one captured HIP graph (``--eager``:
+one launch per call from Python; the eager time is reported too).
+``roofline`` prices the dominant kernel: algorithmic bytes per step
+(distinct adapters' A_i and B_i, 2 r_i (h_in + h_out) bytes each, plus x
+read, y read and written, and the token ids) over that kernel's average
+duration.  Where a step is one launch, that is the step graph's duration
+between two HIP events recorded on the stream the kernels run on; otherwise
+it is the apply's: K plora_apply calls captured as one graph and replayed
+between two such events.  ``cpu_baseline`` times the CPU oracle on a bounded
+sample of the same workload.
 """
 from __future__ import annotations
 
@@ -69,11 +73,12 @@ def source_digest() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(name: str):
-    """HBM bytes per apply launch from the committed counter summary of this
-    workload, or None when there is none or the kernel source has changed
-    since the counters were taken."""
-    path = os.path.join(PROFILES, f"plora_apply_{name}_traffic.txt")
+def measured_traffic(stem: str):
+    """HBM bytes per launch of the priced kernel from the committed counter
+    summary (profiles/<stem>_traffic.txt, stem = kernel and workload), or
+    None when there is none or the kernel source has changed since the
+    counters were taken."""
+    path = os.path.join(PROFILES, f"{stem}_traffic.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -191,10 +196,16 @@ def main():
 
     def step(k, ev=None):
         d = k % len(draws)
-        P.segment(idx_dev[d], segs[d])
         if ev is not None:
             ev[0].record()
-        apply_call(k)
+        if n_proj == 1:
+            # segmentation and apply in one call (one launch for decode-sized
+            # batches; plora_segment then plora_apply otherwise)
+            T = draws[d].size
+            P.segment_apply(idx_dev[d], x[:T], reps[k % R][0], segs[d], ys[0][:T], ws)
+        else:
+            P.segment(idx_dev[d], segs[d])
+            apply_call(k)
         if ev is not None:
             ev[1].record()
 
@@ -212,6 +223,7 @@ def main():
     torch.cuda.synchronize()
     wall_eager = time.perf_counter() - t0
     wall = wall_eager
+    step_event_s = None
 
     # ---- the same K steps launched as one HIP graph ------------------------------
     # At decode size a step's two kernels take less GPU time than Python needs
@@ -225,10 +237,14 @@ def main():
                 step(args.warmup + k)
         graph.replay()
         torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
+        s0.record()
         graph.replay()
+        s1.record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        step_event_s = s0.elapsed_time(s1) / 1e3
 
     apply_ms = np.array([a.elapsed_time(b) for a, b in evs])
     ks = [(args.warmup + k) % len(draws) for k in range(K)]
@@ -271,8 +287,18 @@ def main():
         separate_s = timed(separate=True)
     bytes_total = sum(tot_bytes[k % len(draws)] for k in range(K))
     bytes_adapter = sum(ad_bytes[k % len(draws)] for k in range(K))
-    achieved = bytes_total / apply_s / 1e9
-    traffic = measured_traffic(name) if n_proj == 1 else None
+    # the kernel the roofline prices: where a step is a single launch
+    # (plora_segment_apply's one-launch form) that launch, timed over the
+    # step graph; otherwise the apply's own launches
+    one_launch = (n_proj == 1 and step_event_s is not None and
+                  all(P.plora_segment_apply_launches(d.size, bases[0].struct) == 1
+                      for d in draws))
+    priced_s = step_event_s if one_launch else apply_s
+    kernel = ("segment_apply_kernel (plora_segment_apply)" if one_launch else
+              "plora_apply" if n_proj == 1 else "plora_apply_multi")
+    achieved = bytes_total / priced_s / 1e9
+    traffic = (measured_traffic(("plora_segment_apply_" if one_launch else "plora_apply_") + name)
+               if n_proj == 1 else None)
     adapter_gbps = bytes_adapter / apply_s / 1e9
 
     # ---- same-footprint plain-read ceiling -------------------------------------
@@ -366,7 +392,9 @@ def main():
         "adapter_GBps": round(adapter_gbps, 1),
         "adapter_frac_of_peak": round(adapter_gbps / HBM_PEAK_GBPS, 4),
         "apply_us": round(apply_s / K * 1e6, 3),
-        "apply_us_isolated_events": {
+        "step_us_events": (None if step_event_s is None
+                           else round(step_event_s / K * 1e6, 3)),
+        "step_us_isolated_events": {
             "mean": round(float(apply_ms.mean()) * 1e3, 3),
             "p10": round(float(np.percentile(apply_ms, 10)) * 1e3, 3),
             "p90": round(float(np.percentile(apply_ms, 90)) * 1e3, 3)},
@@ -374,7 +402,8 @@ def main():
         "adapter_bytes_per_launch": int(bytes_adapter / K),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic},
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "kernel": kernel, "us_per_launch": round(priced_s / K * 1e6, 3)},
         "read_ceiling": ceiling,
         "separate_calls_us": (None if separate_s is None
                               else round(separate_s / K * 1e6, 3)),

@@ -263,6 +263,30 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx,
                          hipStream_t stream);
 
 /*
+ * plora_segment followed by plora_apply on the same batch, as one call: the
+ * first projection of a step, which also produces the step's segmentation
+ * (seg is filled exactly as plora_segment fills it, so later projections and
+ * layers can call plora_apply with it).  Arguments as for the two calls;
+ * idx is int32 [T] device memory.  For T <= 64 in plora_apply's split
+ * exchange form (and N < 2^26 - 1) this is one launch: every work group
+ * segments the batch itself, with one wavefront (the grouping of section
+ * VI-B) and applies its own tile, and one of them also writes seg.
+ * Otherwise it makes the two calls.  y gets the bits plora_apply would give
+ * after plora_segment (with the same exception for a partner that never
+ * publishes).  Errors as for the two calls.
+ */
+plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t ldx,
+                                 const plora_adapters* ad, const plora_segments* seg,
+                                 uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+/* Host.  How many launches plora_segment_apply makes for a batch of T
+ * tokens over this stack: 1 (the one-launch form), 2 (plora_segment then
+ * a one-launch plora_apply) or 3 (then a two-launch one); 0 for T <= 0 or
+ * a stack plora_apply would reject. */
+int32_t plora_segment_apply_launches(int32_t T, const plora_adapters* ad);
+
+/*
  * The apply for several projections of one layer that read the same input x
  * and the same token batch (the paper attaches LoRA adapters to the query,
  * key, value and output projections and the FFN, section VII-A; section II-A

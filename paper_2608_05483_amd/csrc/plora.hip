@@ -611,17 +611,11 @@ __device__ __forceinline__ const uint16_t* adapter_block(const uint16_t* dev, in
   return base + e;
 }
 
-// Read and validate tile u.  Returns false (for the whole work group) for
-// padding entries and for adapters the kernels must skip.  Threads below L
-// also fetch their tile row's token index (-1 if unusable); it is issued
-// together with the adapter metadata so both arrive in one trip.
-__device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, int& my_tok) {
-  if (u < 0 || u >= g.tile_cap) return false;
-  const int4 ti = g.tiles[u];
-  t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
-  if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
-    return false;
-  my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
+// Adapter t.a's rank, scale and blocks into t (t.a, t.p0 and t.L already
+// set and checked); false, for the whole work group, for an adapter the
+// kernels must skip.  my_tok (this thread's tile row's token, requested by
+// the caller just before) is cleared to -1 if out of range.
+__device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& my_tok) {
   t.r = g.ranks[t.a];
   const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
   t.s = g.scales[t.a];
@@ -636,6 +630,20 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
   t.j0 = 0;
   t.j1 = g.h_out;
   return true;
+}
+
+// Read and validate tile u.  Returns false (for the whole work group) for
+// padding entries and for adapters the kernels must skip.  Threads below L
+// also fetch their tile row's token index (-1 if unusable); it is issued
+// together with the adapter metadata so both arrive in one trip.
+__device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, int& my_tok) {
+  if (u < 0 || u >= g.tile_cap) return false;
+  const int4 ti = g.tiles[u];
+  t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
+  if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
+    return false;
+  my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
+  return tile_adapter(g, t, my_tok);
 }
 
 // Item i of plan p: items are numbered in groups of eight tiles, slice-major
@@ -1790,16 +1798,17 @@ __device__ __forceinline__ void plain_v(const ApplyArgs& g, const Tile& t, const
 // and epoch in the workspace): the shrink of h_in rows [s KR, (s+1) KR),
 // the exchange of partial v with the tile's other items, and the expand of
 // y columns [s W, (s+1) W), whose first loads of B_i and y are issued with
-// the shrink's.  If the exchange times out, plain_v computes v here.
-__device__ __forceinline__ void apply_item(const ApplyArgs& g, int u, int s, int slot,
-                                           ItemStash& stash, unsigned char* lds) {
+// the shrink's.  If the exchange times out, plain_v computes v here.  ep is
+// the slot's epoch as the caller read it; src(t, my_tok) fills in the tile
+// (adapter, first position, length) and this thread's token, false for a
+// slot without a usable tile.
+template <class Src>
+__device__ __forceinline__ void apply_item(const ApplyArgs& g, int s, int slot, uint64_t ep,
+                                           ItemStash& stash, unsigned char* lds, Src&& src) {
   {
-    // the slot's epoch is requested together with the tile record (the host
-    // made sure slot < kXSlots)
-    const uint64_t ep = u < g.tile_cap ? xload(g.xep + slot) : 0;
     Tile t;
     int my_tok;
-    if (!load_tile(g, u, t, my_tok)) return;
+    if (!src(t, my_tok)) return;
     if (threadIdx.x == 0) {
       stash.a = t.a; stash.p0 = t.p0; stash.L = t.L; stash.r = t.r; stash.s = t.s;
       stash.u = slot; stash.slice = s; stash.Ai = t.Ai; stash.Bi = t.Bi; stash.ep = ep;
@@ -1837,7 +1846,11 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   __shared__ ItemStash stash;
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
-  apply_item(g, u, s, u, stash, apply_lds);
+  // the slot's epoch is requested together with the tile record (the host
+  // made sure the slot count is at most kXSlots)
+  const uint64_t ep = xload(g.xep + u);
+  apply_item(g, s, u, ep, stash, apply_lds,
+             [&](Tile& t, int& my_tok) { return load_tile(g, u, t, my_tok); });
 }
 
 // The per-projection part of a multi-projection apply (see plora_apply_multi).
@@ -1881,7 +1894,140 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void apply_multi_kernel(MultiArgs m)
   g.b_pool_len = q.b_pool_len;
   g.a_off = q.a_off; g.b_off = q.b_off; g.ranks = q.ranks; g.scales = q.scales;
   g.y = q.y; g.ldy = q.ldy; g.h_out = q.h_out; g.max_rank = q.max_rank;
-  apply_item(g, u, s, slot, stash, apply_lds);
+  const uint64_t ep = xload(g.xep + slot);
+  apply_item(g, s, slot, ep, stash, apply_lds,
+             [&](Tile& t, int& my_tok) { return load_tile(g, u, t, my_tok); });
+}
+
+// ---------------------------------------------------------------------------
+// plora_segment_apply: segmentation and the one-launch apply in one launch
+// ---------------------------------------------------------------------------
+
+// Where plora_segment's outputs go (the caller's plora_segments).
+struct SegOut {
+  int32_t* perm;
+  int32_t* seg_ptr;
+  int32_t* seg_id;
+  int32_t* meta;
+  int4* tiles;
+  int32_t cap, tile_cap;
+};
+
+// One work group's tile, as the wavefront segmentation found it (L = 0: the
+// slot has no tile), and the wavefront's sorting space.
+struct LocalTile {
+  int a, p0, L;
+  int tok[kTT];
+  uint32_t words[64];     // word of token t
+  uint32_t sorted[64];    // word at sorted position p
+};
+
+// The segmentation of a batch of T <= 64 tokens by one wavefront, the same
+// function plora_segment computes: tokens ordered by (adapter id, token
+// index), ids outside [0, N) after every valid one.  Each lane holds the
+// word (key << 6) | t of one token (key = id, N for a skipped token, N + 1
+// past T).  The words are distinct, so each one's rank (how many words are
+// smaller, counted against all 64 read back from LDS) is its sorted
+// position, and there is exactly one order.  Segments start where the key
+// changes, tiles every kTT positions into a segment.  With `write`, the
+// wavefront stores every output of plora_segment (perm, seg_ptr, seg_id,
+// tiles and meta, unused tails included); every caller gets tile u in lt.
+// (A bitonic sort over lane shuffles measured about 1 us: 21 dependent
+// cross-lane permutes.)
+__device__ __forceinline__ void wave_segment(const int32_t* idx, int T, int N, int u,
+                                             const SegOut& so, bool write, LocalTile& lt) {
+  const int lane = threadIdx.x & 63;
+  const bool in = lane < T;
+  const int id = in ? idx[lane] : 0;
+  const bool valid = in && id >= 0 && id < N;
+  const bool none = in && id == -1;
+  const bool invalid = in && !valid && !none;
+  const uint32_t key = valid ? (uint32_t)id : (uint32_t)N + (in ? 0u : 1u);
+  const uint32_t w = (key << 6) | (uint32_t)lane;
+  // LDS traffic of one wavefront is processed in order, so each read below
+  // sees every lane's write before it
+  lt.words[lane] = w;
+  __builtin_amdgcn_wave_barrier();
+  int rank = 0;
+#pragma unroll
+  for (int q = 0; q < 64; q += 4) {
+    const uint4 o = *reinterpret_cast<const uint4*>(lt.words + q);
+    rank += (o.x < w) + (o.y < w) + (o.z < w) + (o.w < w);
+  }
+  lt.sorted[rank] = w;
+  __builtin_amdgcn_wave_barrier();
+  const uint32_t sw = lt.sorted[lane];
+  const uint32_t sprev = lt.sorted[lane > 0 ? lane - 1 : 0];
+  const int kp = (int)(sw >> 6), tp = (int)(sw & 63);
+  const uint64_t bit = uint64_t(1) << lane;
+  const uint64_t below = bit - 1, upto = below | bit;
+  const int n_none = __popcll(__ballot(none));
+  const int n_invalid = __popcll(__ballot(invalid));
+  const int n_valid = T - n_none - n_invalid;
+  const bool vp = lane < n_valid;
+  const bool sflag = vp && (lane == 0 || (int)(sprev >> 6) != kp);
+  const uint64_t smask = __ballot(sflag);
+  const int n_seg = __popcll(smask);
+  const int cur = __popcll(smask & upto) - 1;            // segment of position lane
+  const int sstart = vp ? 63 - __clzll(smask & upto) : 0;
+  const uint64_t later = smask & ~upto;
+  const int send = later ? __ffsll((long long)later) - 1 : n_valid;   // segment end
+  const bool tflag = vp && ((lane - sstart) % kTT) == 0;
+  const uint64_t tmask = __ballot(tflag);
+  const int tu = __popcll(tmask & below);                 // tile starting here
+  const int n_tiles = min(__popcll(tmask), so.tile_cap);
+  if (write) {
+    if (in) so.perm[lane] = vp ? tp : -1;
+    if (sflag) {
+      so.seg_ptr[cur] = lane;
+      so.seg_id[cur] = kp;
+    }
+    for (int q = n_seg + lane; q <= so.cap; q += 64) so.seg_ptr[q] = n_valid;
+    for (int q = n_seg + lane; q < so.cap; q += 64) so.seg_id[q] = -1;
+    if (tflag && tu < so.tile_cap) so.tiles[tu] = make_int4(kp, lane, min(kTT, send - lane), cur);
+    for (int q = n_tiles + lane; q < so.tile_cap; q += 64) so.tiles[q] = make_int4(-1, 0, 0, -1);
+    if (lane < 8)
+      so.meta[lane] = lane == 0 ? n_seg : lane == 1 ? n_valid : lane == 2 ? n_none
+                    : lane == 3 ? n_invalid : lane == 4 ? n_tiles : 0;
+  }
+  // tile u starts at the u-th tile start p0 and ends at kTT positions or at
+  // the end of its segment
+  const uint64_t mine = __ballot(tflag && tu == u && u < n_tiles);
+  const int p0 = mine ? __ffsll((long long)mine) - 1 : 0;
+  const uint64_t after0 = smask & (p0 == 63 ? 0 : ~((uint64_t(2) << p0) - 1));
+  const int end0 = after0 ? __ffsll((long long)after0) - 1 : n_valid;
+  const int L = mine ? min(kTT, end0 - p0) : 0;
+  if (lane == 0) {
+    lt.a = (int)(lt.sorted[p0] >> 6);
+    lt.p0 = p0;
+    lt.L = L;
+  }
+  if (lane < kTT) lt.tok[lane] = lane < L ? (int)(lt.sorted[min(p0 + lane, 63)] & 63) : -1;
+}
+
+// plora_segment_apply for T <= 64 in the exchange form: every work group
+// segments the batch itself (reading idx takes the trip the tile record
+// would) and takes its own tile, and work group 0 also writes the
+// segmentation for later calls.  Items are those of apply_kernel.
+__global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs g,
+                                                                      const int32_t* idx,
+                                                                      SegOut so) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  __shared__ LocalTile lt;
+  int u, s;
+  exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
+  const uint64_t ep = xload(g.xep + u);
+  if (threadIdx.x < 64) wave_segment(idx, g.T, g.N, u, so, blockIdx.x == 0, lt);
+  lds_sync();
+  apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {
+    t.a = lt.a;
+    t.p0 = lt.p0;
+    t.L = lt.L;
+    if (t.L <= 0 || t.a < 0 || t.a >= g.N) return false;
+    my_tok = (int)threadIdx.x < t.L ? lt.tok[threadIdx.x] : -1;
+    return tile_adapter(g, t, my_tok);
+  });
 }
 
 // plora_apply as one launch, one slice per tile in h_in: item (tile,
@@ -2162,6 +2308,13 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   return PLORA_OK;
 }
 
+// plora_segment_apply runs as one launch for batches of up to 64 tokens in
+// the exchange form (one wavefront sorts words (key << 6) | t, key <= N + 1).
+bool segment_apply_one_launch(int32_t T, const plora_adapters* ad) {
+  return T <= 64 && ad->n_adapters < (1 << 26) - 1 &&
+         fused_slices(plora_tile_capacity(T, ad->n_adapters), ad->h_in, ad->h_out) > 1;
+}
+
 // Dynamic LDS above 64 KB is opted into once per kernel.
 void allow_lds(const void* kernel, std::atomic<bool>& done) {
   if (done.load()) return;
@@ -2171,7 +2324,7 @@ void allow_lds(const void* kernel, std::atomic<bool>& done) {
 }
 
 std::atomic<bool> g_lds_shrink{false}, g_lds_expand{false}, g_lds_apply{false},
-    g_lds_cols{false}, g_lds_parts{false}, g_lds_multi{false};
+    g_lds_cols{false}, g_lds_parts{false}, g_lds_multi{false}, g_lds_segapply{false};
 
 template <class K>
 plora_status launch_items(K kernel, std::atomic<bool>& lds_done, const ApplyArgs& g,
@@ -2296,6 +2449,41 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   st = launch_items(shrink_part_kernel, g_lds_shrink, g, g.ks_max, stream);
   if (st != PLORA_OK) return st;
   return launch_items(expand_kernel<true>, g_lds_parts, g, g.js_max, stream);
+}
+
+int32_t plora_segment_apply_launches(int32_t T, const plora_adapters* ad) {
+  if (T <= 0 || !ad || check_adapters_host(ad) != PLORA_OK) return 0;
+  if (segment_apply_one_launch(T, ad)) return 1;
+  return fused_for(T) ? 2 : 3;
+}
+
+plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t ldx,
+                                 const plora_adapters* ad, const plora_segments* seg,
+                                 uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  ApplyArgs g;
+  plora_status st = prepare(ad, seg, ws, ws_bytes, g, true);
+  if (st != PLORA_OK) return st;
+  const int32_t T = seg->T;
+  if (T == 0) return PLORA_OK;
+  if (!idx || !x || !y) return PLORA_ERR_INVALID_ARG;
+  if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
+  if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
+  if (!segment_apply_one_launch(T, ad)) {
+    st = plora_segment(idx, seg, ad->n_adapters, ws, ws_bytes, stream);
+    if (st != PLORA_OK) return st;
+    return plora_apply(x, ldx, ad, seg, y, ldy, ws, ws_bytes, stream);
+  }
+  g.x = x; g.ldx = ldx; g.y = y; g.ldy = ldy;
+  const SegOut so{seg->perm, seg->seg_ptr, seg->seg_id, seg->meta,
+                  reinterpret_cast<int4*>(seg->tiles), seg->cap, seg->tile_cap};
+  const size_t lds = smem_bytes(g.h_in, g.max_rank);
+  if (lds > 64 * 1024)
+    allow_lds(reinterpret_cast<const void*>(segment_apply_kernel), g_lds_segapply);
+  clear_stale_error();
+  hipLaunchKernelGGL(segment_apply_kernel, dim3(grid_for(g, g.js_max)), dim3(kNT), lds, stream,
+                     g, idx, so);
+  return launch_status();
 }
 
 size_t plora_workspace_bytes_multi(int32_t T, const plora_adapters* ads, int32_t n_proj) {

@@ -29,6 +29,7 @@ PLORA_MAX_PROJECTIONS = 8
 
 EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_init",
             "plora_segment", "plora_shrink", "plora_expand", "plora_apply",
+            "plora_segment_apply", "plora_segment_apply_launches",
             "plora_apply_multi", "plora_workspace_bytes_multi",
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
@@ -85,6 +86,9 @@ def _load() -> ctypes.CDLL:
     L.plora_shrink.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_expand.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_apply.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_segment_apply.argtypes = [P, P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_segment_apply_launches.argtypes = [i32, AD]
+    L.plora_segment_apply_launches.restype = i32
     L.plora_apply_multi.argtypes = [P, i64, AD, i32, SG, ctypes.POINTER(P),
                                     ctypes.POINTER(i64), P, sz, P]
     L.plora_workspace_bytes_multi.argtypes = [i32, AD, i32]
@@ -99,7 +103,8 @@ def _load() -> ctypes.CDLL:
     L.plora_debug_set_exchange_polls.argtypes = [i32]
     L.plora_debug_set_exchange_polls.restype = None
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
-               "plora_expand", "plora_apply", "plora_apply_multi", "plora_check_adapters"):
+               "plora_expand", "plora_apply", "plora_segment_apply", "plora_apply_multi",
+               "plora_check_adapters"):
         getattr(L, fn).restype = ctypes.c_int
     return L
 
@@ -153,6 +158,17 @@ def plora_apply(x: int, ldx: int, ad: plora_adapters, seg: plora_segments, y: in
                 ldy: int, ws: int, ws_bytes: int, stream: int) -> None:
     _ok("plora_apply", lib.plora_apply(x, ldx, ctypes.byref(ad), ctypes.byref(seg),
                                        y, ldy, ws, ws_bytes, stream))
+
+
+def plora_segment_apply(idx: int, x: int, ldx: int, ad: plora_adapters, seg: plora_segments,
+                        y: int, ldy: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _ok("plora_segment_apply",
+        lib.plora_segment_apply(idx, x, ldx, ctypes.byref(ad), ctypes.byref(seg), y, ldy, ws,
+                                ws_bytes, stream))
+
+
+def plora_segment_apply_launches(T: int, ad: plora_adapters) -> int:
+    return int(lib.plora_segment_apply_launches(T, ctypes.byref(ad)))
 
 
 def _stack_array(ads):
@@ -313,6 +329,12 @@ def expand(v, ad: Adapters, segs: Segments, y, stream=None) -> None:
 def apply(x, ad: Adapters, segs: Segments, y, ws: Workspace, stream=None) -> None:
     plora_apply(x.data_ptr(), x.stride(0), ad.struct, segs.struct, y.data_ptr(),
                 y.stride(0), ws.ptr, ws.nbytes, _stream(stream))
+
+
+def segment_apply(idx, x, ad: Adapters, segs: Segments, y, ws: Workspace, stream=None) -> None:
+    """segment() then apply() on the same batch, as one call."""
+    plora_segment_apply(idx.data_ptr(), x.data_ptr(), x.stride(0), ad.struct, segs.struct,
+                        y.data_ptr(), y.stride(0), ws.ptr, ws.nbytes, _stream(stream))
 
 
 def apply_multi(x, ads, segs: Segments, ys, ws: Workspace, stream=None) -> None:

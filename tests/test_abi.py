@@ -258,3 +258,51 @@ def test_apply_multi_host_checks():
     # an empty batch launches nothing
     empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
     assert _multi_status([a, b], seg=empty, ws=None, ws_bytes=0) == P.PLORA_OK
+
+
+def _segapply_status(ad=None, seg=None, idx=FAKE, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
+                     ws_bytes=None):
+    ad = ad or _ad()
+    seg = seg or _seg()
+    if ws_bytes is None:
+        ws_bytes = P.plora_workspace_bytes(seg.T, ad)
+    return P.lib.plora_segment_apply(idx, x, ldx, ctypes.byref(ad), ctypes.byref(seg), y, ldy,
+                                     ws, ws_bytes, None)
+
+
+def test_segment_apply_host_checks():
+    assert _segapply_status(idx=None) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(x=None) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(y=None) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(ldx=200) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(ldy=260) == P.PLORA_ERR_UNSUPPORTED
+    assert _segapply_status(x=FAKE + 8) == P.PLORA_ERR_UNSUPPORTED
+    assert _segapply_status(ad=_ad(h_out=12)) == P.PLORA_ERR_UNSUPPORTED
+    assert _segapply_status(seg=_seg(cap=3)) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(ws=None) == P.PLORA_ERR_INVALID_ARG
+    assert _segapply_status(ws_bytes=256) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    assert _segapply_status(seg=empty, idx=None, x=None, y=None) == P.PLORA_OK
+
+
+def test_adapter_blocks_must_stay_below_2gib():
+    # adapter blocks are read through 32-bit byte offsets: max(h_in, h_out)
+    # * max_rank * 2 bytes must stay below 2^31 (checked before the empty
+    # batch returns)
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    h = 1 << 23
+    big = _ad(h_in=h, h_out=256, max_rank=128)
+    assert _apply_status(ad=big, seg=empty, ldx=h) == P.PLORA_ERR_UNSUPPORTED
+    ok = _ad(h_in=1 << 22, h_out=256, max_rank=128)
+    assert _apply_status(ad=ok, seg=empty, ldx=1 << 22) == P.PLORA_OK
+
+
+def test_segment_apply_launch_count():
+    dec = _ad(n_adapters=1000, h_in=4096, h_out=4096, max_rank=16)
+    assert P.plora_segment_apply_launches(64, dec) == 1     # decode: one launch
+    assert P.plora_segment_apply_launches(1, dec) == 1
+    assert P.plora_segment_apply_launches(65, dec) == 2     # segment, then one apply launch
+    assert P.plora_segment_apply_launches(4096, dec) == 3   # segment, then two apply launches
+    assert P.plora_segment_apply_launches(8, _ad()) == 2    # h = 256: no split form
+    assert P.plora_segment_apply_launches(0, dec) == 0
+    assert P.plora_segment_apply_launches(8, _ad(h_in=12)) == 0

@@ -105,6 +105,16 @@ class Run:
         torch.cuda.synchronize()
         return bits16(y)[:, :self.w.h_out]
 
+    def segment_apply(self):
+        y = dev(self.y0.view(np.int16))
+        self.P.segment_apply(self.idx_d, self.x, self.ad, self.segs, y, self.ws)
+        torch.cuda.synchronize()
+        return bits16(y)[:, :self.w.h_out]
+
+    def seg_words(self):
+        s = self.segs
+        return torch.cat([s.perm, s.seg_ptr, s.seg_id, s.meta, s.tiles]).cpu().numpy()
+
     def shrink(self, ldv=None):
         ldv = ldv or self.ad.max_rank
         v = torch.full((self.T, ldv), float("nan"), dtype=torch.float32, device="cuda")
@@ -588,3 +598,78 @@ def test_pool_pointer_must_be_pinned(P):
     with pytest.raises(P.PloraError):
         P.plora_pool_device_pointer(t.data_ptr())
     assert P.plora_pool_device_pointer(t.pin_memory().data_ptr()) != 0
+
+
+# ---------------------------------------------------------------------------
+# plora_segment_apply: segmentation and apply in one call
+# ---------------------------------------------------------------------------
+
+def _segapply_cases():
+    """Batches of at most 64 tokens on the decode stack (one launch) and two
+    that take the two-call path (the large config, T = 256, and tiny, whose
+    h = 256 allows no split)."""
+    rng = np.random.default_rng(33)
+    N = W.CONFIGS["decode"].N
+    mixed = rng.integers(0, 6, size=64).astype(np.int32)
+    mixed[rng.choice(64, 9, replace=False)] = -1
+    mixed[rng.choice(64, 5, replace=False)] = N + 7
+    return [
+        ("decode", "decode", None),
+        ("decode_T1", "decode", np.array([417], np.int32)),
+        ("decode_T63_few_ids", "decode", rng.integers(0, 3, size=63).astype(np.int32)),
+        ("decode_one_id_two_tiles", "decode", np.full(64, 5, np.int32)),
+        ("decode_skips_mixed", "decode", mixed),
+        ("decode_all_skipped", "decode", np.full(40, -1, np.int32)),
+        ("decode_desc", "decode", np.arange(64, dtype=np.int32)[::-1].copy() * 15),
+        ("large_two_calls", "large", None),
+        ("tiny_two_calls", "tiny", None),
+    ]
+
+
+@pytest.mark.parametrize("case", range(len(_segapply_cases())),
+                         ids=[c[0] for c in _segapply_cases()])
+@pytest.mark.parametrize("scale", ["paper", "parity"])
+def test_segment_apply_matches_two_calls_and_oracle(P, case, scale):
+    """The segmentation it writes is the oracle's, bit for bit; y is the
+    bits of plora_segment followed by plora_apply, and meets the oracle's
+    bars."""
+    name, cfg, idx = _segapply_cases()[case]
+    w = workload(cfg, scale)
+    if idx is not None:
+        w = W.with_idx(w, idx)
+    say(f"segment_apply {name}/{scale} T={w.T}")
+    run = Run(P, w)
+    run.segs.perm.fill_(-9)
+    run.segs.tiles.fill_(-9)
+    y_f = run.segment_apply()
+    check_segments(P, run, w.n_adapters)
+    words_f = run.seg_words()
+    run.segment()
+    torch.cuda.synchronize()
+    assert (run.seg_words() == words_f).all()
+    y_s = run.apply()
+    assert (y_f == y_s).all()
+    yref, yout = oracle_y(w)
+    any_valid = ((w.idx >= 0) & (w.idx < w.n_adapters)).any()
+    check_y(y_f, yref, yout, w, strict_l2=(scale == "parity" and any_valid))
+
+
+def test_segment_apply_deterministic_in_a_graph(P):
+    """Replays of a captured segment_apply, with eager work between them,
+    give the eager call's bits every time."""
+    w = workload("decode", "paper")
+    run = Run(P, w)
+    y_eager = run.segment_apply()
+    y = dev(run.y0.view(np.int16))
+    y_init = y.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run.P.segment_apply(run.idx_d, run.x, run.ad, run.segs, y, run.ws)
+    for _ in range(4):
+        y.copy_(y_init)
+        run.segs.perm.fill_(-9)
+        g.replay()
+        torch.cuda.synchronize()
+        assert (bits16(y)[:, :w.h_out] == y_eager).all()
+        check_segments(P, run, w.n_adapters)
+        run.apply()          # eager work on the same workspace between replays
