@@ -611,14 +611,13 @@ __device__ __forceinline__ const uint16_t* adapter_block(const uint16_t* dev, in
   return base + e;
 }
 
-// Adapter t.a's rank, scale and blocks into t (t.a, t.p0 and t.L already
-// set and checked); false, for the whole work group, for an adapter the
-// kernels must skip.  my_tok (this thread's tile row's token, requested by
-// the caller just before) is cleared to -1 if out of range.
-__device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& my_tok) {
-  t.r = g.ranks[t.a];
-  const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
-  t.s = g.scales[t.a];
+// Adapter t.a's blocks into t, given its element offsets (t.a, t.p0, t.L,
+// t.r and t.s already set); false, for the whole work group, for an
+// adapter the kernels must skip.  my_tok (this thread's tile row's token)
+// is cleared to -1 if out of range.  tile_adapter below reads the rank,
+// scale and offsets first.
+__device__ __forceinline__ bool tile_blocks(const ApplyArgs& g, Tile& t, int& my_tok,
+                                            int64_t ao, int64_t bo) {
   if (my_tok < 0 || my_tok >= g.T) my_tok = -1;
   // ranks 8, 16, 32, 64, 128 (up to max_rank); anything else is skipped
   if (t.r < 8 || t.r > g.max_rank || (t.r & (t.r - 1))) return false;
@@ -630,6 +629,13 @@ __device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& m
   t.j0 = 0;
   t.j1 = g.h_out;
   return true;
+}
+
+__device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& my_tok) {
+  t.r = g.ranks[t.a];
+  const int64_t ao = g.a_off[t.a], bo = g.b_off[t.a];
+  t.s = g.scales[t.a];
+  return tile_blocks(g, t, my_tok, ao, bo);
 }
 
 // Read and validate tile u.  Returns false (for the whole work group) for
@@ -1916,10 +1922,15 @@ struct SegOut {
 // One work group's tile, as the wavefront segmentation found it (L = 0: the
 // slot has no tile), and the wavefront's sorting space.
 struct LocalTile {
-  int a, p0, L;
+  int a, p0, L, r;
+  float s;
+  int64_t ao, bo;
   int tok[kTT];
   uint32_t words[64];     // word of token t
   uint32_t sorted[64];    // word at sorted position p
+  int rank_of[64];        // rank, scale and offsets of token t's adapter
+  float scale_of[64];
+  int64_t ao_of[64], bo_of[64];
 };
 
 // The segmentation of a batch of T <= 64 tokens by one wavefront, the same
@@ -1934,14 +1945,21 @@ struct LocalTile {
 // tiles and meta, unused tails included); every caller gets tile u in lt.
 // (A bitonic sort over lane shuffles measured about 1 us: 21 dependent
 // cross-lane permutes.)
-__device__ __forceinline__ void wave_segment(const int32_t* idx, int T, int N, int u,
+__device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* idx, int u,
                                              const SegOut& so, bool write, LocalTile& lt) {
+  const int T = g.T, N = g.N;
   const int lane = threadIdx.x & 63;
   const bool in = lane < T;
   const int id = in ? idx[lane] : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
   const bool invalid = in && !valid && !none;
+  // the metadata of this token's adapter, requested now so that its trip
+  // overlaps the ranking (lanes without an adapter read adapter 0's, unused)
+  const int ida = valid ? id : 0;
+  const int m_r = g.ranks[ida];
+  const float m_s = g.scales[ida];
+  const int64_t m_ao = g.a_off[ida], m_bo = g.b_off[ida];
   const uint32_t key = valid ? (uint32_t)id : (uint32_t)N + (in ? 0u : 1u);
   const uint32_t w = (key << 6) | (uint32_t)lane;
   // LDS traffic of one wavefront is processed in order, so each read below
@@ -1997,10 +2015,21 @@ __device__ __forceinline__ void wave_segment(const int32_t* idx, int T, int N, i
   const uint64_t after0 = smask & (p0 == 63 ? 0 : ~((uint64_t(2) << p0) - 1));
   const int end0 = after0 ? __ffsll((long long)after0) - 1 : n_valid;
   const int L = mine ? min(kTT, end0 - p0) : 0;
+  lt.rank_of[lane] = m_r;
+  lt.scale_of[lane] = m_s;
+  lt.ao_of[lane] = m_ao;
+  lt.bo_of[lane] = m_bo;
+  __builtin_amdgcn_wave_barrier();
   if (lane == 0) {
-    lt.a = (int)(lt.sorted[p0] >> 6);
+    const uint32_t s0 = lt.sorted[p0];
+    const int t0 = (int)(s0 & 63);           // the tile's first token: its adapter's metadata
+    lt.a = (int)(s0 >> 6);
     lt.p0 = p0;
     lt.L = L;
+    lt.r = lt.rank_of[t0];
+    lt.s = lt.scale_of[t0];
+    lt.ao = lt.ao_of[t0];
+    lt.bo = lt.bo_of[t0];
   }
   if (lane < kTT) lt.tok[lane] = lane < L ? (int)(lt.sorted[min(p0 + lane, 63)] & 63) : -1;
 }
@@ -2018,15 +2047,20 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   const uint64_t ep = xload(g.xep + u);
-  if (threadIdx.x < 64) wave_segment(idx, g.T, g.N, u, so, blockIdx.x == 0, lt);
+  if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
   lds_sync();
   apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {
-    t.a = lt.a;
-    t.p0 = lt.p0;
-    t.L = lt.L;
+    // wave-uniform values (from LDS the compiler cannot tell), so that the
+    // adapter's metadata and everything derived from it stay scalar
+    t.a = __builtin_amdgcn_readfirstlane(lt.a);
+    t.p0 = __builtin_amdgcn_readfirstlane(lt.p0);
+    t.L = __builtin_amdgcn_readfirstlane(lt.L);
     if (t.L <= 0 || t.a < 0 || t.a >= g.N) return false;
+    t.r = __builtin_amdgcn_readfirstlane(lt.r);
+    t.s = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lt.s)));
+    const int64_t ao = lt.ao, bo = lt.bo;
     my_tok = (int)threadIdx.x < t.L ? lt.tok[threadIdx.x] : -1;
-    return tile_adapter(g, t, my_tok);
+    return tile_blocks(g, t, my_tok, ao, bo);
   });
 }
 
@@ -2309,9 +2343,10 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
 }
 
 // plora_segment_apply runs as one launch for batches of up to 64 tokens in
-// the exchange form (one wavefront sorts words (key << 6) | t, key <= N + 1).
+// the exchange form (one wavefront ranks words (key << 6) | t, key <= N + 1,
+// and reads adapter 0's metadata for tokens without an adapter, so N >= 1).
 bool segment_apply_one_launch(int32_t T, const plora_adapters* ad) {
-  return T <= 64 && ad->n_adapters < (1 << 26) - 1 &&
+  return T <= 64 && ad->n_adapters > 0 && ad->n_adapters < (1 << 26) - 1 &&
          fused_slices(plora_tile_capacity(T, ad->n_adapters), ad->h_in, ad->h_out) > 1;
 }
 
