@@ -60,6 +60,10 @@ def parse():
     ap.add_argument("--projections", type=int, default=1,
                     help="LoRA-injected projections of one layer sharing x, applied "
                          "by one plora_apply_multi call (1: plora_apply)")
+    ap.add_argument("--pool-from", type=int, default=-1, metavar="K",
+                    help="also time the apply with adapters K.. read from a pinned host "
+                         "pool (strategy E2) and the rest from HBM (E1), next to the "
+                         "all-HBM apply, with the cost model's prediction for both")
     ap.add_argument("--eager", action="store_true",
                     help="time the steps as individual launches instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -301,6 +305,51 @@ def main():
                if n_proj == 1 else None)
     adapter_gbps = bytes_adapter / apply_s / 1e9
 
+    # ---- placement split: adapters K.. from the pinned host pool ----------------
+    placement = None
+    if args.pool_from >= 0 and n_proj == 1:
+        from paper_2608_05483_amd import placement as PL
+        Kp = args.pool_from
+        A_pool = torch.from_numpy(w.A.view(np.int16)).pin_memory()
+        B_pool = torch.from_numpy(w.B.view(np.int16)).pin_memory()
+        in_pool = np.arange(N) >= Kp
+        a_off = torch.from_numpy(np.where(in_pool, -1 - w.a_off, w.a_off).astype(np.int64)).to(dev)
+        b_off = torch.from_numpy(np.where(in_pool, -1 - w.b_off, w.b_off).astype(np.int64)).to(dev)
+        pool_reps = [P.Adapters(rp[0].A, rp[0].B, a_off, b_off, rp[0].ranks, rp[0].scales,
+                                w.h_in, w.h_out, w.max_rank, A_pool=A_pool, B_pool=B_pool)
+                     for rp in reps]
+
+        def pool_call(k, separate=False):
+            d = k % len(draws)
+            T = draws[d].size
+            P.apply(x[:T], pool_reps[k % R], segs[d], ys[0][:T], ws)
+
+        saved = apply_call
+        apply_call = pool_call
+        pool_s = timed()
+        apply_call = saved
+        hw = PL.Hardware()
+        model_split, model_hbm, pool_bytes = [], [], []
+        for d in draws:
+            ok = (d >= 0) & (d < N)
+            Bc = np.bincount(d[ok], minlength=N)
+            st = np.where(in_pool, PL.E2, PL.E1).astype(object)
+            model_split.append(PL.lora_time(Bc, w.ranks, st, w.h_in, w.h_out, hw))
+            model_hbm.append(PL.lora_time(Bc, w.ranks, np.full(N, PL.E1, dtype=object),
+                                          w.h_in, w.h_out, hw))
+            pool_bytes.append(sum(PL.adapter_bytes(w.ranks[a], w.h_in, w.h_out)
+                                  for a in np.unique(d[ok]) if a >= Kp))
+        placement = {
+            "pool_from": Kp,
+            "apply_us_split": round(pool_s / K * 1e6, 3),
+            "apply_us_all_hbm": round(apply_s / K * 1e6, 3),
+            "pool_bytes_per_call": int(np.mean(pool_bytes)),
+            "model_us_split": round(float(np.mean(model_split)) * 1e6, 3),
+            "model_us_all_hbm": round(float(np.mean(model_hbm)) * 1e6, 3),
+            "model_hardware": {"C_gpu": hw.C_gpu, "W_gpu": hw.W_gpu, "W_link": hw.W_link,
+                               "L_link": hw.L_link},
+        }
+
     # ---- same-footprint plain-read ceiling -------------------------------------
     ceiling = None
     if not args.no_ceiling and n_proj == 1:
@@ -407,6 +456,7 @@ def main():
         "read_ceiling": ceiling,
         "separate_calls_us": (None if separate_s is None
                               else round(separate_s / K * 1e6, 3)),
+        "placement": placement,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

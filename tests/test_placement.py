@@ -1,0 +1,194 @@
+"""The placement decision (strategies E1 / E2 of section V-A): the cost
+terms against the printed table at h_in = h_out = D and hand-worked values,
+the temperature metric's closed form, and the selection's behaviour and
+invariants.  CPU only."""
+import numpy as np
+import pytest
+
+from paper_2608_05483_amd import placement as PL
+
+HW = PL.Hardware(C_gpu=1.0e3, W_gpu=1.0e2, W_link=1.0e1, L_link=0.5, S=2)
+
+
+def table_e1(B, R, D, hw):
+    """The E1 row as printed, square model dimension D."""
+    B, R = np.asarray(B), np.asarray(R)
+    return max(4 * np.sum(B * D * R) / hw.C_gpu, 2 * D * hw.S * np.sum(R[B > 0]) / hw.W_gpu)
+
+
+def table_e2(B, R, D, hw):
+    B, R = np.asarray(B), np.asarray(R)
+    return max(4 * np.sum(B * D * R) / hw.C_gpu,
+               2 * hw.L_link + 2 * D * hw.S * np.sum(R[B > 0]) / hw.W_link)
+
+
+@pytest.mark.parametrize("B,R,D", [([3, 0, 1], [8, 16, 8], 4), ([0, 0, 5], [8, 8, 64], 16),
+                                   ([100, 200, 0], [8, 16, 32], 2)])
+def test_cost_terms_reduce_to_the_table_at_square_shapes(B, R, D):
+    sel = np.ones(len(B), bool)
+    assert PL.cost_e1(B, R, sel, D, D, HW) == pytest.approx(table_e1(B, R, D, HW))
+    assert PL.cost_e2(B, R, sel, D, D, HW) == pytest.approx(table_e2(B, R, D, HW))
+
+
+def test_cost_terms_hand_worked():
+    # h_in = 8, h_out = 24: flops 2 * B r (h_in + h_out), bytes S r (h_in + h_out)
+    B, R = [2, 0], [8, 16]
+    sel = np.array([True, True])
+    flops = 2 * 2 * 8 * 32            # 1024
+    nbytes = 2 * 8 * 32               # 512 (adapter 1 serves nothing: not read)
+    assert PL.cost_e1(B, R, sel, 8, 24, HW) == pytest.approx(max(flops / 1e3, nbytes / 1e2))
+    assert PL.cost_e2(B, R, sel, 8, 24, HW) == pytest.approx(2 * 0.5 + nbytes / 1e1)
+    # no work, no term (not even the link latency)
+    assert PL.cost_e2([0, 0], R, sel, 8, 24, HW) == 0.0
+    assert PL.cost_e1(B, R, np.array([False, True]), 8, 24, HW) == 0.0
+    # lora_time sums the two strategies' terms
+    st = np.array([PL.E1, PL.E2])
+    assert PL.lora_time([2, 3], R, st, 8, 24, HW) == pytest.approx(
+        PL.cost_e1([2, 3], R, st == PL.E1, 8, 24, HW) +
+        PL.cost_e2([2, 3], R, st == PL.E2, 8, 24, HW))
+
+
+def test_temperature_relaxes_geometrically_and_keeps_the_mean():
+    t = PL.Temperature(5, increment=2.0, relax=0.1)
+    t.request([0, 0, 3])
+    assert t.t.tolist() == [4.0, 0, 0, 2.0, 0]
+    mean = t.t.mean()
+    gap0 = t.t - mean
+    for k in range(1, 8):
+        t.step()
+        assert t.t.mean() == pytest.approx(mean)
+        assert np.allclose(t.t - mean, gap0 * 0.9 ** k)
+    assert t.order([4, 3, 0, 1]).tolist() == [0, 3, 1, 4]   # ties: lower id first
+
+
+def _setup(n=6, rank=8, h=8):
+    ranks = np.full(n, rank)
+    return ranks, PL.adapter_bytes(rank, h, h)
+
+
+def test_unlimited_budget_caches_every_serving_adapter():
+    ranks, sz = _setup()
+    B = np.array([3, 0, 1, 0, 0, 2])
+    t = PL.Temperature(6)
+    d = PL.choose(B, ranks, 8, 8, HW, budget=100 * sz, resident=np.zeros(6, bool), temp=t)
+    assert all(d.strategy[a] == PL.E1 for a in (0, 2, 5))
+    assert set(d.loads) >= {0, 2, 5} and not d.evictions
+    assert d.resident.all()                 # the rest pre-cached (hot list of 50)
+
+
+def test_zero_budget_reads_everything_from_the_pool():
+    ranks, sz = _setup()
+    B = np.array([3, 0, 1, 0, 0, 2])
+    d = PL.choose(B, ranks, 8, 8, HW, budget=0, resident=np.zeros(6, bool),
+                  temp=PL.Temperature(6))
+    assert all(d.strategy[a] == PL.E2 for a in range(6))
+    assert not d.loads and not d.resident.any()
+    assert d.cost == pytest.approx(PL.cost_e2(B, ranks, np.ones(6, bool), 8, 8, HW))
+
+
+def test_a_link_as_fast_as_hbm_needs_no_cache():
+    ranks, sz = _setup()
+    hw = PL.Hardware(C_gpu=1e3, W_gpu=1e2, W_link=1e2, L_link=0.0, S=2)
+    d = PL.choose([1, 2, 0, 0, 0, 0], ranks, 8, 8, hw, budget=0 * sz + 10 ** 9,
+                  resident=np.zeros(6, bool), temp=PL.Temperature(6), n_hot=0)
+    assert d.strategy[0] == PL.E2 and d.strategy[1] == PL.E2 and not d.loads
+
+
+def test_cold_adapters_go_first():
+    ranks, sz = _setup()
+    t = PL.Temperature(6)
+    t.request([4] * 5 + [3] * 2 + [2])      # 4 hottest, then 3, then 2
+    res = np.zeros(6, bool)
+    res[[2, 3, 4]] = True                   # HBM full (budget 3 adapters)
+    B = np.array([5, 0, 0, 0, 0, 0])
+    d = PL.choose(B, ranks, 8, 8, HW, budget=3 * sz, resident=res, temp=t, n_hot=1)
+    # hot = {4}; cold = {3, 2}: the coldest (2) makes room
+    assert d.strategy[0] == PL.E1 and d.evictions == [2]
+    assert d.resident[[0, 3, 4]].all() and not d.resident[2]
+
+
+def test_hot_adapters_go_when_no_cold_one_is_left():
+    ranks, sz = _setup()
+    t = PL.Temperature(6)
+    t.request([4] * 5 + [3] * 4)
+    res = np.zeros(6, bool)
+    res[[3, 4]] = True
+    d = PL.choose([5, 0, 0, 0, 0, 0], ranks, 8, 8, HW, budget=2 * sz, resident=res, temp=t,
+                  n_hot=2)
+    # both cached adapters are hot; E1 evicting the cooler one beats E2
+    assert d.strategy[0] == PL.E1 and d.evictions == [3]
+
+
+def test_evicting_a_serving_adapter_only_when_the_model_says_so():
+    ranks, sz = _setup()
+    t = PL.Temperature(6)
+    res = np.zeros(6, bool)
+    res[1] = True                            # serving adapter 1 holds all of HBM
+    B = np.array([5, 5, 0, 0, 0, 0])
+    d = PL.choose(B, ranks, 8, 8, HW, budget=sz, resident=res, temp=t)
+    # swapping 0 in and 1 out costs the same as reading 0 from the pool: keep
+    assert d.strategy[0] == PL.E2 and d.strategy[1] == PL.E1 and not d.evictions
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_selection_invariants(seed):
+    rng = np.random.default_rng(seed)
+    n = 40
+    ranks = rng.choice([8, 16, 32, 64], size=n)
+    h_in, h_out = 64, 32
+    # the host link is slower than HBM (the only regime that arises; with a
+    # faster link, keeping a cached adapter on E1 is not the best choice and
+    # the greedy selection makes no promise)
+    hw = PL.Hardware(C_gpu=1e6, W_gpu=1e4, W_link=rng.choice([1e2, 1e3, 5e3]),
+                     L_link=rng.choice([0.0, 0.01]), S=2)
+    t = PL.Temperature(n)
+    budget = int(rng.integers(0, 12)) * PL.adapter_bytes(32, h_in, h_out)
+    res = np.zeros(n, bool)
+    size = np.array([PL.adapter_bytes(r, h_in, h_out) for r in ranks])
+    for step in range(6):
+        ids = rng.integers(0, n, size=int(rng.integers(1, 30)))
+        t.request(ids)
+        B = np.bincount(ids, minlength=n)
+        d = PL.choose(B, ranks, h_in, h_out, hw, budget, res, t, n_hot=5)
+        assert size[d.resident].sum() <= budget
+        for a in range(n):
+            assert (d.strategy[a] == PL.E1) == bool(d.resident[a])
+        assert not set(d.loads) & set(d.evictions)
+        assert all(not res[a] and d.resident[a] for a in d.loads)
+        assert all(res[a] and not d.resident[a] for a in d.evictions)
+        assert d.cost == pytest.approx(PL.lora_time(B, ranks, d.strategy, h_in, h_out, hw))
+        # never worse than reading every serving adapter from the pool
+        all_e2 = np.full(n, PL.E2, dtype=object)
+        assert d.cost <= PL.lora_time(B, ranks, all_e2, h_in, h_out, hw) + 1e-12
+        res = d.resident
+        t.step()
+
+
+def test_hbm_cache_places_blocks_and_names_them():
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(3)
+    n, h_in, h_out = 7, 16, 8
+    ranks = np.array([8, 16, 8, 32, 8, 16, 8])
+    a_off = np.concatenate([[0], np.cumsum(h_in * ranks)[:-1]]).astype(np.int64)
+    b_off = np.concatenate([[0], np.cumsum(h_out * ranks)[:-1]]).astype(np.int64)
+    A = torch.from_numpy(rng.integers(-1000, 1000, int(np.sum(h_in * ranks))).astype(np.int16))
+    Bp = torch.from_numpy(rng.integers(-1000, 1000, int(np.sum(h_out * ranks))).astype(np.int16))
+    budget = 3 * PL.adapter_bytes(16, h_in, h_out)
+    cache = PL.HbmCache(A, Bp, a_off, b_off, ranks, h_in, h_out, budget, device="cpu")
+    res = np.zeros(n, bool)
+    t = PL.Temperature(n)
+    for B in ([2, 0, 1, 0, 0, 0, 0], [0, 3, 0, 1, 0, 0, 2], [0, 0, 0, 0, 4, 4, 0]):
+        t.request(np.repeat(np.arange(n), B))
+        d = PL.choose(np.array(B), ranks, h_in, h_out, PL.Hardware(), budget, res, t, n_hot=2)
+        cache.apply(d)
+        ao, bo = cache.offsets()
+        for a in range(n):
+            na, nb = h_in * ranks[a], h_out * ranks[a]
+            if d.resident[a]:
+                assert ao[a] >= 0 and bo[a] >= 0
+                assert torch.equal(cache.A[ao[a]:ao[a] + na], A[a_off[a]:a_off[a] + na])
+                assert torch.equal(cache.B[bo[a]:bo[a] + nb], Bp[b_off[a]:b_off[a] + nb])
+            else:
+                assert ao[a] == -1 - a_off[a] and bo[a] == -1 - b_off[a]
+        res = d.resident
+        t.step()
