@@ -64,6 +64,9 @@ def parse():
                     help="also time the apply with adapters K.. read from a pinned host "
                          "pool (strategy E2) and the rest from HBM (E1), next to the "
                          "all-HBM apply, with the cost model's prediction for both")
+    ap.add_argument("--workload", default="apply", choices=["apply", "attention"],
+                    help="attention: the split-KV decode attention (plora_attn_decode) at "
+                         "Llama-2-7B decode shape instead of the LoRA apply")
     ap.add_argument("--eager", action="store_true",
                     help="time the steps as individual launches instead of one graph")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -123,6 +126,89 @@ def describe(name, c):
             f"N={c.N} bf16 adapters, ids {dist}")
 
 
+def bench_attention(args):
+    """plora_attn_decode on 64 requests x 32 heads x head dim 128 with caches
+    of U{512..4096} keys (seeded), one HBM-resident bf16 KV cache per step
+    replica; K steps captured as one graph and replayed between HIP events."""
+    import torch
+    from paper_2608_05483_amd import plora as P
+    dev = torch.device("cuda:0")
+    Bn, H, D, Lmax = 64, 32, P.ATTN_HEAD_DIM, 4096
+    rng = np.random.default_rng(2024)
+    lens_np = rng.integers(512, Lmax + 1, Bn).astype(np.int32)
+    g = torch.Generator(device=dev).manual_seed(2024)
+    bits = lambda t: t.to(torch.bfloat16).view(torch.int16)
+    R = 2                                     # 2 x 4.3 GB of caches: far past the 256 MB MALL
+    caches = [(bits(torch.randn((Bn, H, Lmax, D), device=dev, generator=g)),
+               bits(torch.randn((Bn, H, Lmax, D), device=dev, generator=g))) for _ in range(R)]
+    q = bits(torch.randn((Bn, H, D), device=dev, generator=g))
+    lens = torch.from_numpy(lens_np).to(dev)
+    out = torch.zeros((Bn, H, D), dtype=torch.int16, device=dev)
+    ws = torch.empty(P.attn_workspace_bytes(Bn, H, Lmax), dtype=torch.uint8, device=dev)
+    scale = 1.0 / math.sqrt(D)
+
+    def step(k):
+        K, V = caches[k % R]
+        P.attn_decode(q, K, V, lens, scale, out, ws)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+    Ks = args.steps
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for k in range(Ks):
+            step(k)
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev = e0.elapsed_time(e1) / 1e3
+    kv_bytes = int(lens_np.sum()) * H * D * 2 * 2
+    step_bytes = kv_bytes + 2 * Bn * H * D * 2
+    achieved = step_bytes / (ev / Ks) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        sys.path.insert(0, ROOT)
+        from oracle import attention as OA
+        Kh = caches[0][0][:2].cpu().numpy().view(np.uint16)
+        Vh = caches[0][1][:2].cpu().numpy().view(np.uint16)
+        qh = q[:2].cpu().numpy().view(np.uint16)
+        n_done, t_cpu = 0, 0.0
+        while t_cpu < args.cpu_seconds:
+            t1 = time.perf_counter()
+            OA.attention(qh, Kh, Vh, lens_np[:2], scale)
+            t_cpu += time.perf_counter() - t1
+            n_done += 1
+        cpu = {"value": round(n_done * 2 / t_cpu, 2), "unit": "requests/s (32 heads each)",
+               "cores": 1, "kind": "oracle",
+               "sample": f"{n_done} passes over requests 0 and 1 of this batch "
+                         f"(caches of {int(lens_np[0])} and {int(lens_np[1])} keys), "
+                         f"float64 numpy oracle, {t_cpu:.1f} s"}
+    print(json.dumps({
+        "metric": "decode attention KV-cache GB/s (% of HBM peak), split-KV with exact merge",
+        "value": round(Bn * Ks / wall, 1), "unit": "requests/s (32 heads each)",
+        "n_gpus": 1, "steps": Ks, "warmup": args.warmup,
+        "ms_per_step": round(wall / Ks * 1e3, 5), "launch": "hip graph of the K steps",
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"decode attention: {Bn} requests x {H} heads x head dim {D}, "
+                               f"caches U{{512..{Lmax}}} keys (seeded), bf16",
+                   "batch": Bn, "heads": H, "head_dim": D, "max_len": Lmax,
+                   "kv_keys": int(lens_np.sum()), "cache_replicas": R},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": None, "kernel": "attn_partial_kernel + attn_merge_kernel",
+                     "us_per_launch": round(ev / Ks * 1e6, 3)},
+        "bytes_per_step": step_bytes,
+        "cpu_baseline": cpu}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -132,6 +218,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration > 0:
         copy_calibration(args.copy_calibration)
+        return
+    if args.workload == "attention":
+        bench_attention(args)
         return
 
     import torch

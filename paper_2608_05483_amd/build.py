@@ -8,6 +8,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "plora.hip")
+ATTN_SRC = os.path.join(PKG, "csrc", "attention.hip")
 PROBE_SRC = os.path.join(PKG, "csrc", "read_ceiling.hip")
 HEADER = os.path.join(ROOT, "include", "plora.h")
 LIB = os.path.join(PKG, "libplora.so")
@@ -20,9 +21,10 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-Wall", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 
-def _hipcc(src: str, out: str, verbose: bool) -> str:
+def _hipcc(srcs, out: str, verbose: bool) -> str:
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), src, "-o", tmp]
+    srcs = [srcs] if isinstance(srcs, str) else list(srcs)
+    cmd = [HIPCC, *FLAGS, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
@@ -37,7 +39,7 @@ def _hipcc(src: str, out: str, verbose: bool) -> str:
 def build(verbose: bool = False) -> str:
     """Compile every HIP source of the package (always recompiles): the
     product library and the read-ceiling probe the benchmark reports."""
-    _hipcc(SRC, LIB, verbose)
+    _hipcc([SRC, ATTN_SRC], LIB, verbose)
     _hipcc(PROBE_SRC, PROBE_LIB, verbose)
     return LIB
 

@@ -33,7 +33,10 @@ EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_ini
             "plora_apply_multi", "plora_workspace_bytes_multi",
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
-            "plora_pool_device_pointer")
+            "plora_pool_device_pointer",
+            # include/plora_attention.h
+            "plora_attn_partitions", "plora_attn_workspace_bytes", "plora_attn_partial",
+            "plora_attn_merge", "plora_attn_decode")
 
 
 class PloraError(RuntimeError):
@@ -102,6 +105,16 @@ def _load() -> ctypes.CDLL:
     L.plora_pool_device_pointer.restype = ctypes.c_int
     L.plora_debug_set_exchange_polls.argtypes = [i32]
     L.plora_debug_set_exchange_polls.restype = None
+    L.plora_attn_partitions.argtypes = [i64]
+    L.plora_attn_partitions.restype = i32
+    L.plora_attn_workspace_bytes.argtypes = [i32, i32, i64]
+    L.plora_attn_workspace_bytes.restype = sz
+    F = ctypes.c_float
+    L.plora_attn_partial.argtypes = [P, P, P, P, i32, i32, i64, F, P, P, P, P]
+    L.plora_attn_merge.argtypes = [P, P, P, P, i32, i32, i64, P, P]
+    L.plora_attn_decode.argtypes = [P, P, P, P, i32, i32, i64, F, P, P, sz, P]
+    for fn in ("plora_attn_partial", "plora_attn_merge", "plora_attn_decode"):
+        getattr(L, fn).restype = ctypes.c_int
     for fn in ("plora_workspace_init", "plora_segment", "plora_shrink",
                "plora_expand", "plora_apply", "plora_segment_apply", "plora_apply_multi",
                "plora_check_adapters"):
@@ -335,6 +348,45 @@ def segment_apply(idx, x, ad: Adapters, segs: Segments, y, ws: Workspace, stream
     """segment() then apply() on the same batch, as one call."""
     plora_segment_apply(idx.data_ptr(), x.data_ptr(), x.stride(0), ad.struct, segs.struct,
                         y.data_ptr(), y.stride(0), ws.ptr, ws.nbytes, _stream(stream))
+
+
+# ---- split-KV decode attention (include/plora_attention.h) --------------------
+
+ATTN_HEAD_DIM = 128
+ATTN_CHUNK = 256
+
+
+def attn_partitions(max_len: int) -> int:
+    return int(lib.plora_attn_partitions(max_len))
+
+
+def attn_workspace_bytes(batch: int, heads: int, max_len: int) -> int:
+    return int(lib.plora_attn_workspace_bytes(batch, heads, max_len))
+
+
+def attn_partial(q, k, v, lens, scale: float, m, l, o, stream=None) -> None:
+    """q [B, H, 128], k / v [B, H, Lmax, 128] (bf16 bits as int16 tensors),
+    lens int32 [B]; m, l float32 [B, H, P], o float32 [B, H, P, 128]."""
+    Bn, H, Lmax = k.shape[0], k.shape[1], k.shape[2]
+    _ok("plora_attn_partial", lib.plora_attn_partial(
+        q.data_ptr(), k.data_ptr(), v.data_ptr(), lens.data_ptr(), Bn, H, Lmax, scale,
+        m.data_ptr(), l.data_ptr(), o.data_ptr(), _stream(stream)))
+
+
+def attn_merge(m, l, o, lens, out, max_len: int, stream=None) -> None:
+    Bn, H = m.shape[0], m.shape[1]
+    _ok("plora_attn_merge", lib.plora_attn_merge(
+        m.data_ptr(), l.data_ptr(), o.data_ptr(), lens.data_ptr(), Bn, H, max_len,
+        out.data_ptr(), _stream(stream)))
+
+
+def attn_decode(q, k, v, lens, scale: float, out, ws, stream=None) -> None:
+    """ws: a uint8 tensor of at least attn_workspace_bytes bytes."""
+    Bn, H, Lmax = k.shape[0], k.shape[1], k.shape[2]
+    _ok("plora_attn_decode", lib.plora_attn_decode(
+        q.data_ptr(), k.data_ptr(), v.data_ptr(), lens.data_ptr(), Bn, H, Lmax, scale,
+        out.data_ptr(), ws.data_ptr() if ws is not None else None,
+        ws.numel() if ws is not None else 0, _stream(stream)))
 
 
 def apply_multi(x, ads, segs: Segments, ys, ws: Workspace, stream=None) -> None:

@@ -10,14 +10,14 @@ import pytest
 from paper_2608_05483_amd import build as B
 from paper_2608_05483_amd import plora as P
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                      "include", "plora.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+HEADERS = [os.path.join(INCLUDE, h) for h in ("plora.h", "plora_attention.h")]
 
 FAKE = 0x10000  # an aligned non-null address; never dereferenced by these checks
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(plora_[a-z_]+)\s*\(", text)))
 
@@ -306,3 +306,30 @@ def test_segment_apply_launch_count():
     assert P.plora_segment_apply_launches(8, _ad()) == 2    # h = 256: no split form
     assert P.plora_segment_apply_launches(0, dec) == 0
     assert P.plora_segment_apply_launches(8, _ad(h_in=12)) == 0
+
+
+def test_attention_host_checks():
+    L = P.lib
+    assert P.attn_partitions(0) == 0 and P.attn_partitions(1) == 1
+    assert P.attn_partitions(256) == 1 and P.attn_partitions(257) == 2
+    assert P.attn_workspace_bytes(0, 32, 100) == 0
+    # m and l: 2 x 3 x 2 floats each, 256-aligned; o: 12 x 128 floats
+    assert P.attn_workspace_bytes(2, 3, 300) == 256 + 256 + 12 * 128 * 4
+    args = dict(q=FAKE, k=FAKE, v=FAKE, lens=FAKE, B=2, H=4, Lm=300)
+
+    def partial(**kw):
+        a = {**args, **kw}
+        return L.plora_attn_partial(a["q"], a["k"], a["v"], a["lens"], a["B"], a["H"], a["Lm"],
+                                    0.1, FAKE, FAKE, FAKE, None)
+    assert partial(q=None) == P.PLORA_ERR_INVALID_ARG
+    assert partial(B=-1) == P.PLORA_ERR_INVALID_ARG
+    assert partial(k=FAKE + 2) == P.PLORA_ERR_UNSUPPORTED
+    assert partial(Lm=1 << 23) == P.PLORA_ERR_UNSUPPORTED   # 2^23 x 256 B per cache
+    assert partial(B=0, q=None) == P.PLORA_OK
+    ws = P.attn_workspace_bytes(2, 4, 300)
+    dec = lambda ws_p, n: L.plora_attn_decode(FAKE, FAKE, FAKE, FAKE, 2, 4, 300, 0.1, FAKE,
+                                              ws_p, n, None)
+    assert dec(None, ws) == P.PLORA_ERR_INVALID_ARG
+    assert dec(FAKE, ws - 1) == P.PLORA_ERR_WORKSPACE_TOO_SMALL
+    assert L.plora_attn_merge(None, FAKE, FAKE, FAKE, 2, 4, 300, FAKE, None) == \
+        P.PLORA_ERR_INVALID_ARG
