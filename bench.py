@@ -498,11 +498,35 @@ def main():
             t_cpu += time.perf_counter() - t1
             toks += d.size
             n_done += 1
+        # the same oracle on one thread, over a tenth of the time
+        t1_cpu, toks1, k1 = 0.0, 0, 0
+        while t1_cpu < args.cpu_seconds / 10:
+            d = draws[k1 % len(draws)]
+            wd = w if d.size == w.T else W.with_idx(w, d)
+            t1 = time.perf_counter()
+            for wp in wps:
+                oracle.apply(wd.x, d, wp.A, wp.a_off, wp.B, wp.b_off, wp.ranks, wp.scales,
+                             np.zeros((d.size, wp.h_out), np.uint16), w.h_in, wp.h_out,
+                             n_threads=1)
+            t1_cpu += time.perf_counter() - t1
+            toks1 += d.size
+            k1 += 1
+        model = "unknown"
+        try:
+            for line in open("/proc/cpuinfo"):
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+        except OSError:
+            pass
         cpu = {"value": round(toks / t_cpu, 1), "unit": "tokens/s", "cores": cores,
                "kind": "oracle",
+               "value_1_thread": round(toks1 / t1_cpu, 1),
+               "cpu_model": model,
                "sample": f"{n_done} batches of this workload, cycling its "
                          f"{len(draws)} token draws ({toks} tokens, {t_cpu:.1f} s), "
-                         f"fp32 C oracle, OpenMP over tokens"}
+                         f"fp32 C oracle, OpenMP over tokens on {cores} threads; "
+                         f"one thread: {k1} batches ({toks1} tokens, {t1_cpu:.1f} s)"}
 
     out = {
         "metric": "tokens/s and effective adapter GB/s (% of HBM peak) for plora_apply",
