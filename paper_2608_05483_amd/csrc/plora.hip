@@ -1921,16 +1921,18 @@ struct SegOut {
 
 // One work group's tile, as the wavefront segmentation found it (L = 0: the
 // slot has no tile), and the wavefront's sorting space.
+constexpr int kSegApplyMax = 256;         // largest batch of the one-launch form
+
 struct LocalTile {
-  int a, p0, L, r;
-  float s;
-  int64_t ao, bo;
-  int tok[kTT];
-  uint32_t words[64];     // word of token t
-  uint32_t sorted[64];    // word at sorted position p
-  int rank_of[64];        // rank, scale and offsets of token t's adapter
-  float scale_of[64];
-  int64_t ao_of[64], bo_of[64];
+  int a, p0, L, t0;       // adapter, first position, length, first token
+  uint32_t tmask;         // token bits of a word
+  int wcount[2][kNT / 64];             // per wavefront: segment and tile starts
+  int wlast[kNT / 64], wfirst[kNT / 64];   // its last and first segment start
+  uint32_t words[kSegApplyMax];        // word of token t
+  uint32_t sorted[kSegApplyMax];       // word at sorted position p
+  int rank_of[kSegApplyMax];           // rank, scale and offsets of token t's adapter
+  float scale_of[kSegApplyMax];
+  int64_t ao_of[kSegApplyMax], bo_of[kSegApplyMax];
 };
 
 // The segmentation of a batch of T <= 64 tokens by one wavefront, the same
@@ -2019,25 +2021,126 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   lt.scale_of[lane] = m_s;
   lt.ao_of[lane] = m_ao;
   lt.bo_of[lane] = m_bo;
-  __builtin_amdgcn_wave_barrier();
   if (lane == 0) {
     const uint32_t s0 = lt.sorted[p0];
-    const int t0 = (int)(s0 & 63);           // the tile's first token: its adapter's metadata
     lt.a = (int)(s0 >> 6);
     lt.p0 = p0;
     lt.L = L;
-    lt.r = lt.rank_of[t0];
-    lt.s = lt.scale_of[t0];
-    lt.ao = lt.ao_of[t0];
-    lt.bo = lt.bo_of[t0];
+    lt.t0 = (int)(s0 & 63);        // the tile's first token: its adapter's metadata
+    lt.tmask = 63u;
   }
-  if (lane < kTT) lt.tok[lane] = lane < L ? (int)(lt.sorted[min(p0 + lane, 63)] & 63) : -1;
 }
 
-// plora_segment_apply for T <= 64 in the exchange form: every work group
-// segments the batch itself (reading idx takes the trip the tile record
-// would) and takes its own tile, and work group 0 also writes the
-// segmentation for later calls.  Items are those of apply_kernel.
+// The same function for 64 < T <= kSegApplyMax tokens by the whole work
+// group (kNT threads, thread t holds token t, then sorted position t).
+// Words are (key << 8) | t; segment and tile starts are found with each
+// wavefront's ballots and combined across the wavefronts through LDS
+// (counts for the indices, the last and first start for the segment that
+// spans a wavefront boundary).  Every thread of the work group calls it.
+__device__ __forceinline__ void block_segment(const ApplyArgs& g, const int32_t* idx, int u,
+                                              const SegOut& so, bool write, LocalTile& lt) {
+  constexpr int NW = kNT / 64;
+  const int T = g.T, N = g.N;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const bool in = tid < T;
+  const int id = in ? idx[tid] : 0;
+  const bool valid = in && id >= 0 && id < N;
+  const bool none = in && id == -1;
+  const bool invalid = in && !valid && !none;
+  const int ida = valid ? id : 0;
+  const int m_r = g.ranks[ida];
+  const float m_s = g.scales[ida];
+  const int64_t m_ao = g.a_off[ida], m_bo = g.b_off[ida];
+  const uint32_t key = valid ? (uint32_t)id : (uint32_t)N + (in ? 0u : 1u);
+  const uint32_t w = (key << 8) | (uint32_t)tid;
+  lt.words[tid] = w;
+  if (tid == 0) lt.L = 0;
+  const int n_none = __syncthreads_count(none);
+  const int n_invalid = __syncthreads_count(invalid);
+  int rank = 0;
+#pragma unroll 8
+  for (int q = 0; q < kNT; q += 4) {
+    const uint4 o = *reinterpret_cast<const uint4*>(lt.words + q);
+    rank += (o.x < w) + (o.y < w) + (o.z < w) + (o.w < w);
+  }
+  lt.sorted[rank] = w;
+  lds_sync();
+  const uint32_t sw = lt.sorted[tid];
+  const uint32_t sprev = lt.sorted[tid > 0 ? tid - 1 : 0];
+  const int kp = (int)(sw >> 8), tp = (int)(sw & 255);
+  const int n_valid = T - n_none - n_invalid;
+  const bool vp = tid < n_valid;
+  const bool sflag = vp && (tid == 0 || (int)(sprev >> 8) != kp);
+  const uint64_t bit = uint64_t(1) << lane;
+  const uint64_t below = bit - 1, upto = below | bit;
+  const uint64_t smask = __ballot(sflag);
+  if (lane == 0) {
+    lt.wcount[0][wv] = __popcll(smask);
+    lt.wlast[wv] = smask ? 64 * wv + 63 - __clzll(smask) : -1;
+    lt.wfirst[wv] = smask ? 64 * wv + __ffsll((long long)smask) - 1 : kNT;
+  }
+  lds_sync();
+  int seg_before = 0, n_seg = 0, last_before = -1, first_after = kNT;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    n_seg += lt.wcount[0][k];
+    if (k < wv) {
+      seg_before += lt.wcount[0][k];
+      last_before = max(last_before, lt.wlast[k]);
+    } else if (k > wv) {
+      first_after = min(first_after, lt.wfirst[k]);
+    }
+  }
+  const int cur = seg_before + __popcll(smask & upto) - 1;   // segment of position tid
+  const int sstart = (smask & upto) ? 64 * wv + 63 - __clzll(smask & upto) : last_before;
+  const uint64_t later = smask & ~upto;
+  int send = later ? 64 * wv + __ffsll((long long)later) - 1 : first_after;
+  send = min(send, n_valid);                                  // segment end
+  const bool tflag = vp && ((tid - sstart) % kTT) == 0;
+  const uint64_t tmask_w = __ballot(tflag);
+  if (lane == 0) lt.wcount[1][wv] = __popcll(tmask_w);
+  lds_sync();
+  int tiles_before = 0, n_tiles_all = 0;
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    n_tiles_all += lt.wcount[1][k];
+    if (k < wv) tiles_before += lt.wcount[1][k];
+  }
+  const int tu = tiles_before + __popcll(tmask_w & below);  // tile starting here
+  const int n_tiles = min(n_tiles_all, so.tile_cap);
+  const int tlen = min(kTT, send - tid);
+  if (write) {
+    if (in) so.perm[tid] = vp ? tp : -1;
+    if (sflag) {
+      so.seg_ptr[cur] = tid;
+      so.seg_id[cur] = kp;
+    }
+    for (int q = n_seg + tid; q <= so.cap; q += kNT) so.seg_ptr[q] = n_valid;
+    for (int q = n_seg + tid; q < so.cap; q += kNT) so.seg_id[q] = -1;
+    if (tflag && tu < so.tile_cap) so.tiles[tu] = make_int4(kp, tid, tlen, cur);
+    for (int q = n_tiles + tid; q < so.tile_cap; q += kNT) so.tiles[q] = make_int4(-1, 0, 0, -1);
+    if (tid < 8)
+      so.meta[tid] = tid == 0 ? n_seg : tid == 1 ? n_valid : tid == 2 ? n_none
+                   : tid == 3 ? n_invalid : tid == 4 ? n_tiles : 0;
+  }
+  lt.rank_of[tid] = m_r;
+  lt.scale_of[tid] = m_s;
+  lt.ao_of[tid] = m_ao;
+  lt.bo_of[tid] = m_bo;
+  if (tflag && tu == u && u < n_tiles) {     // tile u starts here
+    lt.a = kp;
+    lt.p0 = tid;
+    lt.L = tlen;
+    lt.t0 = tp;
+    lt.tmask = 255u;
+  }
+}
+
+// plora_segment_apply for T <= kSegApplyMax in the exchange form: every
+// work group segments the batch itself (reading idx takes the trip the tile
+// record would; one wavefront for T <= 64, the whole group above) and takes
+// its own tile, and work group 0 also writes the segmentation for later
+// calls.  Items are those of apply_kernel.
 __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs g,
                                                                       const int32_t* idx,
                                                                       SegOut so) {
@@ -2047,7 +2150,11 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   const uint64_t ep = xload(g.xep + u);
-  if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
+  if (g.T <= 64) {
+    if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
+  } else {
+    block_segment(g, idx, u, so, blockIdx.x == 0, lt);
+  }
   lds_sync();
   apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {
     // wave-uniform values (from LDS the compiler cannot tell), so that the
@@ -2056,10 +2163,12 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
     t.p0 = __builtin_amdgcn_readfirstlane(lt.p0);
     t.L = __builtin_amdgcn_readfirstlane(lt.L);
     if (t.L <= 0 || t.a < 0 || t.a >= g.N) return false;
-    t.r = __builtin_amdgcn_readfirstlane(lt.r);
-    t.s = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lt.s)));
-    const int64_t ao = lt.ao, bo = lt.bo;
-    my_tok = (int)threadIdx.x < t.L ? lt.tok[threadIdx.x] : -1;
+    const int t0 = __builtin_amdgcn_readfirstlane(lt.t0);
+    t.r = __builtin_amdgcn_readfirstlane(lt.rank_of[t0]);
+    t.s = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lt.scale_of[t0])));
+    const int64_t ao = lt.ao_of[t0], bo = lt.bo_of[t0];
+    const int p = t.p0 + (int)threadIdx.x;
+    my_tok = (int)threadIdx.x < t.L ? (int)(lt.sorted[p < kSegApplyMax ? p : 0] & lt.tmask) : -1;
     return tile_blocks(g, t, my_tok, ao, bo);
   });
 }
@@ -2342,11 +2451,13 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
   return PLORA_OK;
 }
 
-// plora_segment_apply runs as one launch for batches of up to 64 tokens in
-// the exchange form (one wavefront ranks words (key << 6) | t, key <= N + 1,
-// and reads adapter 0's metadata for tokens without an adapter, so N >= 1).
+// plora_segment_apply runs as one launch for batches of up to kSegApplyMax
+// tokens in the exchange form (words (key << tbits) | t with key <= N + 1
+// and tbits 6 up to 64 tokens, 8 above; tokens without an adapter read
+// adapter 0's metadata, so N >= 1).
 bool segment_apply_one_launch(int32_t T, const plora_adapters* ad) {
-  return T <= 64 && ad->n_adapters > 0 && ad->n_adapters < (1 << 26) - 1 &&
+  const int32_t n_limit = T <= 64 ? (1 << 26) - 1 : (1 << 24) - 1;
+  return T <= kSegApplyMax && ad->n_adapters > 0 && ad->n_adapters < n_limit &&
          fused_slices(plora_tile_capacity(T, ad->n_adapters), ad->h_in, ad->h_out) > 1;
 }
 

@@ -605,15 +605,25 @@ def test_pool_pointer_must_be_pinned(P):
 # ---------------------------------------------------------------------------
 
 def _segapply_cases():
-    """Batches of at most 64 tokens on the decode stack (one launch) and two
-    that take the two-call path (the large config, T = 256, and tiny, whose
+    """Batches of up to 256 tokens on the decode stack and the large config
+    (one launch: one wavefront segments up to 64 tokens, the whole work group
+    above), and two that take the two-call path (300 tokens, and tiny, whose
     h = 256 allows no split)."""
     rng = np.random.default_rng(33)
     N = W.CONFIGS["decode"].N
     mixed = rng.integers(0, 6, size=64).astype(np.int32)
     mixed[rng.choice(64, 9, replace=False)] = -1
     mixed[rng.choice(64, 5, replace=False)] = N + 7
+    mixed200 = rng.integers(0, 12, size=200).astype(np.int32)
+    mixed200[rng.choice(200, 30, replace=False)] = -1
+    mixed200[rng.choice(200, 11, replace=False)] = -3
     return [
+        ("decode_T65", "decode", rng.integers(0, N, size=65).astype(np.int32)),
+        ("decode_T200_skips_mixed", "decode", mixed200),
+        ("decode_T200_one_id_seven_tiles", "decode", np.full(200, 9, np.int32)),
+        ("decode_T256_zipf", "decode", W.zipf_ids(rng, 256, N, 1.0)),
+        ("decode_T256_all_skipped", "decode", np.full(256, -1, np.int32)),
+        ("decode_T300_two_calls", "decode", rng.integers(0, N, size=300).astype(np.int32)),
         ("decode", "decode", None),
         ("decode_T1", "decode", np.array([417], np.int32)),
         ("decode_T63_few_ids", "decode", rng.integers(0, 3, size=63).astype(np.int32)),
@@ -621,7 +631,7 @@ def _segapply_cases():
         ("decode_skips_mixed", "decode", mixed),
         ("decode_all_skipped", "decode", np.full(40, -1, np.int32)),
         ("decode_desc", "decode", np.arange(64, dtype=np.int32)[::-1].copy() * 15),
-        ("large_two_calls", "large", None),
+        ("large", "large", None),
         ("tiny_two_calls", "tiny", None),
     ]
 
