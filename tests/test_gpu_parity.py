@@ -624,6 +624,9 @@ def _segapply_cases():
         ("decode_T256_zipf", "decode", W.zipf_ids(rng, 256, N, 1.0)),
         ("decode_T256_all_skipped", "decode", np.full(256, -1, np.int32)),
         ("decode_T300_two_calls", "decode", rng.integers(0, N, size=300).astype(np.int32)),
+        # the ragged stack (ranks 8..64 side by side) through both segmenting forms
+        ("ragged_T64_mixed_ranks", "ragged", W.zipf_ids(rng, 64, N, 0.8)),
+        ("ragged_T200_mixed_ranks", "ragged", W.zipf_ids(rng, 200, N, 0.8)),
         ("decode", "decode", None),
         ("decode_T1", "decode", np.array([417], np.int32)),
         ("decode_T63_few_ids", "decode", rng.integers(0, 3, size=63).astype(np.int32)),
