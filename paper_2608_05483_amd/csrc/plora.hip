@@ -140,15 +140,18 @@ __device__ int block_exscan(int v, int* total, int* sh /* [NW + 1] */) {
 // Batches of T <= NT tokens, one thread per token.  Token t's key is its
 // adapter id, N for skipped tokens; its position in the grouping is the
 // number of keys below it plus the number of equal keys of earlier tokens
-// (a stable sort by key, then token index).  Segment and tile starts are then
+// (a stable sort by key, then token index).  With the distinct words
+// (key << tbits) | t (tbits = ceil(log2 T); the host has checked that
+// N << tbits fits 32 bits) that is the number of words below the token's
+// own, counted four words per LDS read.  Segment and tile starts are then
 // flagged per position and numbered by block scans.
 template <int NT>
 __global__ __launch_bounds__(NT) void segment_small_kernel(
     const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t cap,
-    int32_t tile_cap, int32_t* __restrict__ perm, int32_t* __restrict__ seg_ptr,
+    int32_t tile_cap, int32_t tbits, int32_t* __restrict__ perm, int32_t* __restrict__ seg_ptr,
     int32_t* __restrict__ seg_id, int32_t* __restrict__ meta, int4* __restrict__ tiles) {
   constexpr int NW = NT / 64;
-  __shared__ int32_t key_t[NT];       // key of token t
+  __shared__ __align__(16) uint32_t word_t[NT];   // word of token t
   __shared__ int32_t key_p[NT];       // key at grouped position p
   __shared__ int32_t start_s[NT + 1]; // segment starts, then n_valid
   __shared__ int32_t scan_sh[NW + 1];
@@ -166,17 +169,21 @@ __global__ __launch_bounds__(NT) void segment_small_kernel(
       invalid = !none;
     }
   }
-  key_t[t] = key;
+  const uint32_t word = ((uint32_t)key << tbits) | (uint32_t)t;   // ranked only for t < T
+  word_t[t] = word;
   const int n_none = __syncthreads_count(none);
   const int n_invalid = __syncthreads_count(invalid);
   const int n_valid = T - n_none - n_invalid;
 
   if (t < T) {
     int rank = 0;
-    for (int u = 0; u < T; ++u) {
-      const int k = key_t[u];
-      rank += (k < key || (k == key && u < t)) ? 1 : 0;
+    const int T4 = T & ~3;
+#pragma unroll 4
+    for (int u = 0; u < T4; u += 4) {
+      const uint4 o = *reinterpret_cast<const uint4*>(word_t + u);
+      rank += (o.x < word) + (o.y < word) + (o.z < word) + (o.w < word);
     }
+    for (int u = T4; u < T; ++u) rank += word_t[u] < word;
     key_p[rank] = key;
     perm[rank] = key < N ? t : -1;
   }
@@ -1530,6 +1537,62 @@ __device__ __forceinline__ void expand_prefetch(const ApplyArgs& g, const Tile& 
   expand_load_y<MT>(g, t, t.j0, JC, toks, pre);
 }
 
+// Output words of this wave's first NJ j tiles of a staged chunk (j tile
+// w + i kW for i < NJ): D^T[j][token] = sum_c B_i[c][j] v[token][c] over the
+// K extent rk, v as its bf16 high and low halves, then y = bf16(y + s D).
+// The body is straight-line: every K step reads v's operands once for all j
+// tiles and issues the transposed B_i reads of all NJ tiles before their
+// MFMAs, so LDS latency is paid once per K step rather than once per j tile.
+// Tiles past the chunk (jt >= njt) read the chunk's last tile and their
+// words are never stored.
+template <int NJ, int MT>
+__device__ __forceinline__ void expand_jtiles(const uint16_t* Bs, int S, const uint16_t* vhi,
+                                              const uint16_t* vlo, int RK, int rk, int w,
+                                              int njt, float s, const ExpandPre<MT>& pre,
+                                              uint2 (&out)[kJT][MT]) {
+  const int lane = threadIdx.x & 63, grp = lane >> 4;
+  f32x4_t acc[NJ][MT];
+#pragma unroll
+  for (int i = 0; i < NJ; ++i)
+#pragma unroll
+    for (int nt = 0; nt < MT; ++nt) acc[i][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int kc = 0; kc < rk; kc += kRK) {
+    uint4 h[MT], lo[MT];
+#pragma unroll
+    for (int nt = 0; nt < MT; ++nt) {
+      const int tt = nt * 16 + (lane & 15);
+      h[nt] = *reinterpret_cast<const uint4*>(vhi + tt * RK + kc + 8 * grp);
+      lo[nt] = *reinterpret_cast<const uint4*>(vlo + tt * RK + kc + 8 * grp);
+    }
+    bf16x8_t a[NJ];
+#pragma unroll
+    for (int i = 0; i < NJ; ++i) a[i] = tr_operand(Bs, S, kc, min(w + i * kW, njt - 1) * 16);
+#pragma unroll
+    for (int i = 0; i < NJ; ++i)
+#pragma unroll
+      for (int nt = 0; nt < MT; ++nt) {
+        acc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], as_bf16x8(h[nt]), acc[i][nt], 0, 0, 0);
+        acc[i][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], as_bf16x8(lo[nt]), acc[i][nt], 0, 0, 0);
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < kJT; ++i)
+#pragma unroll
+    for (int nt = 0; nt < MT; ++nt) {
+      if (i < NJ) {
+        const uint2 yw = pre.yv[i][nt];
+        const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
+        const uint32_t o0 = to_bf16(fmaf(s, acc[i < NJ ? i : 0][nt][0], y0));
+        const uint32_t o1 = to_bf16(fmaf(s, acc[i < NJ ? i : 0][nt][1], y1));
+        const uint32_t o2 = to_bf16(fmaf(s, acc[i < NJ ? i : 0][nt][2], y2));
+        const uint32_t o3 = to_bf16(fmaf(s, acc[i < NJ ? i : 0][nt][3], y3));
+        out[i][nt] = make_uint2(o0 | (o1 << 16), o2 | (o3 << 16));
+      } else {
+        out[i][nt] = make_uint2(0, 0);
+      }
+    }
+}
+
 // Expand of a multi-token tile with MT token tiles of 16: D^T[j][token] =
 // sum_c B_i[c][j] (vhi + vlo)[token][c], then y = bf16(y + s D).  Unless
 // `fetched` (expand_prefetch already requested them), the first chunk's
@@ -1589,38 +1652,10 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     // guards hide the exact count from it), which serialised one store
     // round trip per j tile
     uint2 out[kJT][MT];
-#pragma unroll
-    for (int i = 0; i < kJT; ++i) {
-      const int jt = w + i * kW;
-#pragma unroll
-      for (int nt = 0; nt < MT; ++nt) out[i][nt] = make_uint2(0, 0);
-      if (jt < njt) {
-        f32x4_t acc[MT];
-#pragma unroll
-        for (int nt = 0; nt < MT; ++nt) acc[nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-        for (int kc = 0; kc < rk; kc += kRK) {
-          const bf16x8_t a = tr_operand(Bs, S, kc, jt * 16);
-#pragma unroll
-          for (int nt = 0; nt < MT; ++nt) {
-            const int tt = nt * 16 + (lane & 15);
-            const uint4 h = *reinterpret_cast<const uint4*>(vhi + tt * RK + kc + 8 * grp);
-            const uint4 lo = *reinterpret_cast<const uint4*>(vlo + tt * RK + kc + 8 * grp);
-            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_bf16x8(h), acc[nt], 0, 0, 0);
-            acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, as_bf16x8(lo), acc[nt], 0, 0, 0);
-          }
-        }
-#pragma unroll
-        for (int nt = 0; nt < MT; ++nt) {
-          const uint2 yw = pre.yv[i][nt];
-          const float y0 = bf_lo(yw.x), y1 = bf_hi(yw.x), y2 = bf_lo(yw.y), y3 = bf_hi(yw.y);
-          const uint32_t o0 = to_bf16(fmaf(t.s, acc[nt][0], y0));
-          const uint32_t o1 = to_bf16(fmaf(t.s, acc[nt][1], y1));
-          const uint32_t o2 = to_bf16(fmaf(t.s, acc[nt][2], y2));
-          const uint32_t o3 = to_bf16(fmaf(t.s, acc[nt][3], y3));
-          out[i][nt] = make_uint2(o0 | (o1 << 16), o2 | (o3 << 16));
-        }
-      }
-    }
+    const int nj = (njt - w + kW - 1) / kW;          // this wave's j tiles
+    if (nj > 4) expand_jtiles<8, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
+    else if (nj > 2) expand_jtiles<4, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
+    else expand_jtiles<2, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
 #pragma unroll
     for (int i = 0; i < kJT; ++i) {
       const int jt = w + i * kW;
@@ -2529,15 +2564,15 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg, int32_
   int4* tiles = reinterpret_cast<int4*>(seg->tiles);
   if (T <= 64)
     hipLaunchKernelGGL(segment_small_kernel<64>, dim3(1), dim3(64), 0, stream, idx, T,
-                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       n_adapters, seg->cap, seg->tile_cap, tbits, seg->perm, seg->seg_ptr,
                        seg->seg_id, seg->meta, tiles);
   else if (T <= 256)
     hipLaunchKernelGGL(segment_small_kernel<256>, dim3(1), dim3(256), 0, stream, idx, T,
-                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       n_adapters, seg->cap, seg->tile_cap, tbits, seg->perm, seg->seg_ptr,
                        seg->seg_id, seg->meta, tiles);
   else if (T <= 1024)
     hipLaunchKernelGGL(segment_small_kernel<1024>, dim3(1), dim3(1024), 0, stream, idx, T,
-                       n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                       n_adapters, seg->cap, seg->tile_cap, tbits, seg->perm, seg->seg_ptr,
                        seg->seg_id, seg->meta, tiles);
   else
     hipLaunchKernelGGL(segment_kernel, dim3(1), dim3(kSegThreads), 0, stream, idx, T,
