@@ -1192,6 +1192,21 @@ struct NoHook {
   __device__ void operator()() const {}
 };
 
+// Shrink of ranks of 32 and more.  An item's slice of A_i is then long
+// enough that B_i and y requested with it delay it, so where a hook follows
+// (the exchange) they are requested once the shrink is done, to travel
+// during the hook.
+template <int R_OCT, int TG>
+__device__ __forceinline__ void shrink_late(const ApplyArgs& g, const Tile& t, const Smem& sm,
+                                            uint4 (&bpre)[bp_depth<TG>()], uint4 (&ypre)[TG],
+                                            bool do_expand, bool hooked) {
+  shrink_valu<R_OCT, TG>(g, t, sm, bpre, ypre, do_expand && !hooked);
+  if (do_expand && hooked) {
+    prefetch_b<bp_depth<TG>()>(g, t, bpre);
+    prefetch_y<TG>(g, t, sm.tok, ypre);
+  }
+}
+
 template <int TG, class H>
 __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, const Smem& sm,
                                              bool do_shrink, bool do_expand, bool hooked,
@@ -1204,9 +1219,9 @@ __device__ __forceinline__ void valu_tile_tg(const ApplyArgs& g, const Tile& t, 
     switch (t.r >> 3) {
       case 1: shrink_valu<1, TG>(g, t, sm, bpre, ypre, do_expand); break;
       case 2: shrink_valu<2, TG>(g, t, sm, bpre, ypre, do_expand); break;
-      case 4: shrink_valu<4, TG>(g, t, sm, bpre, ypre, do_expand); break;
-      case 8: shrink_valu<8, TG>(g, t, sm, bpre, ypre, do_expand); break;
-      default: shrink_valu<16, TG>(g, t, sm, bpre, ypre, do_expand); break;
+      case 4: shrink_late<4, TG>(g, t, sm, bpre, ypre, do_expand, hooked); break;
+      case 8: shrink_late<8, TG>(g, t, sm, bpre, ypre, do_expand, hooked); break;
+      default: shrink_late<16, TG>(g, t, sm, bpre, ypre, do_expand, hooked); break;
     }
     if (hooked) hook();
   } else {
