@@ -356,15 +356,26 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   const int n_none = n_none_sh, n_invalid = n_invalid_sh;
   const int n_valid = T - n_none - n_invalid;
 
-  // blocked positions per thread
+  // perm in grouped order, one coalesced pass
+  for (int p = tid; p < T; p += kSegThreads)
+    perm[p] = p < n_valid ? (int32_t)(buf0[p] & tmask) : -1;
+
+  // blocked positions per thread; the key of the position before this
+  // thread's first is read once and then carried along
   const int per = (T + kSegThreads - 1) / kSegThreads;
   const int p_begin = tid * per;
+  const uint32_t key_before =
+      p_begin > 0 && p_begin - 1 < n_valid ? buf0[p_begin - 1] >> tbits : 0xffffffffu;
   int nflags = 0;
-  for (int i = 0; i < per; ++i) {
-    int p = p_begin + i;
-    if (p < n_valid) {
-      uint32_t k = buf0[p] >> tbits;
-      if (p == 0 || (buf0[p - 1] >> tbits) != k) ++nflags;
+  {
+    uint32_t prev = key_before;
+    for (int i = 0; i < per; ++i) {
+      const int p = p_begin + i;
+      if (p < n_valid) {
+        const uint32_t k = buf0[p] >> tbits;
+        if (p == 0 || prev != k) ++nflags;
+        prev = k;
+      }
     }
   }
   int n_seg;
@@ -373,12 +384,12 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   int32_t* seg_lds_ptr = reinterpret_cast<int32_t*>(buf1);
   {
     int s = sbase;
+    uint32_t prev = key_before;
     for (int i = 0; i < per; ++i) {
-      int p = p_begin + i;
-      if (p < T) perm[p] = p < n_valid ? (int32_t)(buf0[p] & tmask) : -1;
+      const int p = p_begin + i;
       if (p < n_valid) {
-        uint32_t k = buf0[p] >> tbits;
-        if (p == 0 || (buf0[p - 1] >> tbits) != k) {
+        const uint32_t k = buf0[p] >> tbits;
+        if (p == 0 || prev != k) {
           if (s < cap) {
             seg_ptr[s] = p;
             seg_id[s] = (int32_t)k;
@@ -386,6 +397,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
           }
           ++s;
         }
+        prev = k;
       }
     }
   }
