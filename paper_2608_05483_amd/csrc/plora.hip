@@ -28,6 +28,7 @@
 namespace {
 
 constexpr int kTT = PLORA_TILE_TOKENS;   // tokens per tile
+static_assert((kTT & (kTT - 1)) == 0, "tile positions are taken modulo kTT with a mask");
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
 constexpr int kCH = 8;                   // 16-byte chunks per lane per batch
@@ -410,30 +411,34 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   // tiles: a position starts a tile when it lies a multiple of kTT past its
   // segment's start.  sbase segments start before this thread's first
   // position, so that position belongs to segment sbase - 1 unless it starts
-  // segment sbase itself.
+  // segment sbase itself.  Each thread carries its current segment's start
+  // and the next segment's start (seg_lds_ptr[n_seg] = n_valid ends the
+  // last one) and reads seg_lds_ptr only where a segment begins; cur + 1 <=
+  // n_seg throughout, and cur = -1 only until position 0 starts segment 0.
+  const int start0 = sbase > 0 ? seg_lds_ptr[sbase - 1] : 0;
+  const int next0 = seg_lds_ptr[sbase];
   int ntf = 0;
   {
-    int cur = sbase - 1;
+    int cur = sbase - 1, start = start0, next = next0;
     for (int i = 0; i < per; ++i) {
-      int p = p_begin + i;
+      const int p = p_begin + i;
       if (p < n_valid) {
-        if (cur + 1 < n_seg && seg_lds_ptr[cur + 1] == p) ++cur;
-        if (((p - seg_lds_ptr[cur]) % kTT) == 0) ++ntf;
+        if (p == next) { ++cur; start = next; next = seg_lds_ptr[cur + 1]; }
+        if (((p - start) & (kTT - 1)) == 0) ++ntf;
       }
     }
   }
-  int cur = sbase - 1;
   int n_tiles;
   int tbase = block_exscan(ntf, &n_tiles, scan_sh);
   {
     int tu = tbase;
+    int cur = sbase - 1, start = start0, next = next0;
     for (int i = 0; i < per; ++i) {
-      int p = p_begin + i;
+      const int p = p_begin + i;
       if (p < n_valid) {
-        if (cur + 1 < n_seg && seg_lds_ptr[cur + 1] == p) ++cur;
-        const int start = seg_lds_ptr[cur], end = seg_lds_ptr[cur + 1];
-        if (((p - start) % kTT) == 0) {
-          const int len = min(kTT, end - p);
+        if (p == next) { ++cur; start = next; next = seg_lds_ptr[cur + 1]; }
+        if (((p - start) & (kTT - 1)) == 0) {
+          const int len = min(kTT, next - p);
           if (tu < tile_cap) tiles[tu] = make_int4((int)(buf0[p] >> tbits), p, len, cur);
           ++tu;
         }
