@@ -31,6 +31,9 @@ constexpr int kTT = PLORA_TILE_TOKENS;   // tokens per tile
 static_assert((kTT & (kTT - 1)) == 0, "tile positions are taken modulo kTT with a mask");
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
+// Groups of 64 words per wave in the radix passes: each wave owns a chunk of
+// ceil(T / kSegWaves) words rounded up to 64, at most this many groups.
+constexpr int kSegGroups = ((PLORA_MAX_TOKENS + kSegWaves - 1) / kSegWaves + 63) / 64;
 constexpr int kCH = 8;                   // 16-byte chunks per lane per batch
 constexpr size_t kMaxLds = 160 * 1024;   // LDS per CU on gfx950
 
@@ -298,17 +301,28 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
     const int shift = tbits + pass * dbits;
     for (int d = lane; d < nbuck; d += 64) cursor[w][d] = 0;
     __syncthreads();
-    // count digits per wave
-    for (int g = 0; g < chunk; g += 64) {
-      const int e = e_begin + g + lane;
-      const bool act = e < T;
-      const uint32_t dig = act ? (buf0[e] >> shift) & (uint32_t)(nbuck - 1) : 0u;
-      uint64_t peers = __ballot(act);
-      for (int b = 0; b < dbits; ++b) {
-        uint64_t m = __ballot((dig >> b) & 1u);
-        peers &= ((dig >> b) & 1u) ? m : ~m;
+    // count digits per wave; each group's words and peer masks stay in
+    // registers for the scatter below (a wave has at most kSegGroups groups)
+    uint32_t gword[kSegGroups];
+    uint64_t gpeers[kSegGroups];
+#pragma unroll
+    for (int gi = 0; gi < kSegGroups; ++gi) {
+      gword[gi] = 0u;
+      gpeers[gi] = 0ull;
+      if (gi * 64 < chunk) {
+        const int e = e_begin + gi * 64 + lane;
+        const bool act = e < T;
+        const uint32_t word = act ? buf0[e] : 0u;
+        const uint32_t dig = (word >> shift) & (uint32_t)(nbuck - 1);
+        uint64_t peers = __ballot(act);
+        for (int b = 0; b < dbits; ++b) {
+          uint64_t m = __ballot((dig >> b) & 1u);
+          peers &= ((dig >> b) & 1u) ? m : ~m;
+        }
+        gword[gi] = word;
+        gpeers[gi] = peers;
+        if (act && (peers & below) == 0ull) cursor[w][dig] += __popcll(peers);
       }
-      if (act && (peers & below) == 0ull) cursor[w][dig] += __popcll(peers);
     }
     __syncthreads();
     // exclusive scan in (digit, wave) order
@@ -334,21 +348,20 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
     }
     __syncthreads();
     // stable scatter: groups of 64 in order, rank by lower peers
-    for (int g = 0; g < chunk; g += 64) {
-      const int e = e_begin + g + lane;
-      const bool act = e < T;
-      const uint32_t word = act ? buf0[e] : 0u;
-      const uint32_t dig = (word >> shift) & (uint32_t)(nbuck - 1);
-      uint64_t peers = __ballot(act);
-      for (int b = 0; b < dbits; ++b) {
-        uint64_t m = __ballot((dig >> b) & 1u);
-        peers &= ((dig >> b) & 1u) ? m : ~m;
+#pragma unroll
+    for (int gi = 0; gi < kSegGroups; ++gi) {
+      if (gi * 64 < chunk) {
+        const int e = e_begin + gi * 64 + lane;
+        const bool act = e < T;
+        const uint32_t word = gword[gi];
+        const uint32_t dig = (word >> shift) & (uint32_t)(nbuck - 1);
+        const uint64_t peers = gpeers[gi];
+        const int base = act ? cursor[w][dig] : 0;
+        if (act) buf1[base + __popcll(peers & below)] = word;
+        __builtin_amdgcn_wave_barrier();
+        if (act && (peers & below) == 0ull) cursor[w][dig] = base + __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
       }
-      const int base = act ? cursor[w][dig] : 0;
-      if (act) buf1[base + __popcll(peers & below)] = word;
-      __builtin_amdgcn_wave_barrier();
-      if (act && (peers & below) == 0ull) cursor[w][dig] = base + __popcll(peers);
-      __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
     uint32_t* tmp = buf0; buf0 = buf1; buf1 = tmp;
