@@ -69,10 +69,13 @@
  * T == 0 launches nothing, writes nothing and returns PLORA_OK.
  * Conditions only the device can see never trap: a token whose idx is -1
  * (no adapter) or outside [0, N) keeps y_base and is counted in meta; an
- * adapter whose rank is 0 is a no-op; an adapter whose rank is not a
- * power of two in 8..max_rank, or whose A_i/B_i block is misaligned or runs
- * past a_len/b_len is skipped (its tokens keep y_base) --
- * plora_check_adapters reports such entries on the host.
+ * adapter whose rank is 0 is a no-op.  Every rank from 1 to max_rank is
+ * applied (the paper's range is 2..128, section V-A).  An adapter entry
+ * that breaks the contract -- a rank below 0 or above max_rank, or an
+ * A_i/B_i block that is misaligned or runs past a_len/b_len -- cannot be
+ * applied: its tokens keep y_base and are counted in the workspace
+ * (plora_workspace_counters), and plora_check_adapters reports the first
+ * such entry on the host.
  * Calls that share a workspace or a segments struct must not overlap in time
  * (same stream, or externally ordered).
  */
@@ -117,20 +120,23 @@ typedef enum {
  *   A, B        flat bf16 stacks of a_len and b_len elements in device memory
  *   a_off,b_off int64 [N] element offsets of A_i and B_i (multiples of 8);
  *               an offset o < 0 names element -1 - o of the pool instead
- *   ranks       int32 [N], r_i in {0, 8, 16, 32, 64, 128}, r_i <= max_rank
+ *   ranks       int32 [N], 0 <= r_i <= max_rank (0: a no-op adapter)
  *   scales      fp32  [N], s_i
  *   A_pool, B_pool, a_pool_len, b_pool_len
  *               optional flat bf16 stacks in pinned host memory that the
  *               kernels read directly, element counts (NULL / 0 if unused):
  *               the pooled-memory placement of section V-A, where the GPU
- *               loads A_i and B_i over the link itself (strategy E2); see
- *               include/plora_placement.h for choosing what stays in device
- *               memory.  A and B may be NULL when every offset is negative.
+ *               loads A_i and B_i over the link itself (strategy E2); the
+ *               Python module paper_2608_05483_amd.placement chooses what
+ *               stays in device memory.  A and B may be NULL when every
+ *               offset is negative.
  * Appended fields default to zero in C aggregate initialisation, so callers
  * without pools need not set them.
- * Other ranks (the paper's range is 2..128 and its evaluation draws from
- * {8, 16, 32, 64, 128}) are stored zero-padded to the next of these sizes:
- * zero columns of A_i and zero rows of B_i leave every result unchanged.
+ * Ranks that are multiples of 8 run the vector and matrix-core paths of the
+ * next power of two with their own row stride; other ranks (rows of A_i
+ * that are not 16-byte aligned) take an LDS-staged shrink, correct but not
+ * tuned.  Offsets are multiples of 8 for every rank when h_in and h_out
+ * are, as back-to-back blocks give.
  */
 typedef struct {
   int32_t n_adapters;
@@ -191,7 +197,8 @@ int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 /* Host.  Bytes of device workspace plora_apply and plora_shrink need for a
  * batch of up to T tokens over this adapter stack; 0 for T <= 0.  Three
  * sections, each starting on a 256-byte boundary:
- *   1. the epochs of the one-launch apply's tile slots: 336 64-bit words;
+ *   1. the epochs of the one-launch apply's tile slots: 336 64-bit words,
+ *      then two 64-bit counters (see plora_workspace_counters);
  *   2. its exchange regions: 8 * 32 * 128 64-bit words for each of
  *      P = min(336, max(8, cap8)) tile slots, cap8 being
  *      plora_tile_capacity(T, N) rounded up to a multiple of 8;
@@ -326,8 +333,8 @@ size_t plora_workspace_bytes_multi(int32_t T, const plora_adapters* ads, int32_t
 /*
  * Host, synchronous (copies ranks and offsets to the host and waits on
  * stream).  Returns PLORA_OK if every adapter entry is usable by the kernels
- * (rank 0 or a power of two in 8..max_rank; offsets multiples of 8; blocks
- * inside a_len / b_len), else PLORA_ERR_INVALID_ARG with the first bad
+ * (0 <= rank <= max_rank; offsets multiples of 8; blocks inside a_len /
+ * b_len or the pools), else PLORA_ERR_INVALID_ARG with the first bad
  * adapter index in *bad_index (may be NULL).  Not for the hot path.
  */
 plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
@@ -338,6 +345,22 @@ plora_status plora_check_adapters(const plora_adapters* ad, int32_t* bad_index,
  * address inside the allocation.  PLORA_ERR_UNSUPPORTED if the memory is not
  * pinned and mapped for the device (kernels must never be handed it). */
 plora_status plora_pool_device_pointer(const void* host, const void** device);
+
+/* Host, synchronous (copies two words and waits on stream).  The counters
+ * a workspace keeps since plora_workspace_init zeroed it, summed over every
+ * call made with it:
+ *   counts[0]  one-launch work items whose exchange partners did not publish
+ *              in time, so that they computed v alone (their calls' bits can
+ *              differ in the last places; see plora_apply);
+ *   counts[1]  tokens that kept y_base because their adapter entry breaks
+ *              the contract (a rank outside [0, max_rank], or a block
+ *              misaligned or outside its array), counted once per call;
+ *              plora_expand counts only when it is given a workspace.
+ * PLORA_ERR_INVALID_ARG for null pointers, PLORA_ERR_WORKSPACE_TOO_SMALL for
+ * a buffer that cannot be a workspace, PLORA_ERR_HIP for a failed copy.
+ * Not for the hot path. */
+plora_status plora_workspace_counters(const void* ws, size_t ws_bytes, int64_t* counts,
+                                      hipStream_t stream);
 
 /* Static string naming a status code. */
 const char* plora_status_string(plora_status status);

@@ -1,0 +1,28 @@
+// k_apply.hip -- plora_apply as one launch with the slice exchange.
+#include "plora_dev.h"
+
+namespace plora_impl {
+
+// plora_apply as one launch, tiles in S > 1 slices (S chosen on the host, so
+// the item needs no count from the device): work group blockIdx.x is slice
+// s of tile u, tile slot u, as exchange_item numbers them, so the work
+// groups a tile waits on are dispatched with it.
+__global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  int u, s;
+  exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
+  // the slot's epoch is requested together with the tile record (the host
+  // made sure the slot count is at most kXSlots)
+  const uint64_t ep = xload(g.xep + u);
+  apply_item(g, s, u, ep, stash, apply_lds,
+             [&](Tile& t, int& my_tok) { return load_tile(g, u, t, my_tok); });
+}
+
+void launch_apply(const ApplyArgs& g, unsigned grid, size_t lds, hipStream_t stream) {
+  static std::atomic<bool> lds_done{false};
+  if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(apply_kernel), lds_done);
+  hipLaunchKernelGGL(apply_kernel, dim3(grid), dim3(kNT), lds, stream, g);
+}
+
+}  // namespace plora_impl

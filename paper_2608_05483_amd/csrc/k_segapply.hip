@@ -1,0 +1,50 @@
+// k_segapply.hip -- plora_segment_apply as one launch.
+#include "plora_dev.h"
+
+namespace plora_impl {
+
+// plora_segment_apply for T <= kSegApplyMax in the exchange form: every
+// work group segments the batch itself (reading idx takes the trip the tile
+// record would; one wavefront for T <= 64, the whole group above) and takes
+// its own tile, and work group 0 also writes the segmentation for later
+// calls.  Items are those of apply_kernel.
+__global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs g,
+                                                                      const int32_t* idx,
+                                                                      SegOut so) {
+  extern __shared__ __align__(16) unsigned char apply_lds[];
+  __shared__ ItemStash stash;
+  __shared__ LocalTile lt;
+  int u, s;
+  exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
+  const uint64_t ep = xload(g.xep + u);
+  if (g.T <= 64) {
+    if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
+  } else {
+    block_segment(g, idx, u, so, blockIdx.x == 0, lt);
+  }
+  lds_sync();
+  apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {
+    // wave-uniform values (from LDS the compiler cannot tell), so that the
+    // adapter's metadata and everything derived from it stay scalar
+    t.a = __builtin_amdgcn_readfirstlane(lt.a);
+    t.p0 = __builtin_amdgcn_readfirstlane(lt.p0);
+    t.L = __builtin_amdgcn_readfirstlane(lt.L);
+    if (t.L <= 0 || t.a < 0 || t.a >= g.N) return false;
+    const int t0 = __builtin_amdgcn_readfirstlane(lt.t0);
+    t.r = __builtin_amdgcn_readfirstlane(lt.rank_of[t0]);
+    t.s = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(lt.scale_of[t0])));
+    const int64_t ao = lt.ao_of[t0], bo = lt.bo_of[t0];
+    const int p = t.p0 + (int)threadIdx.x;
+    my_tok = (int)threadIdx.x < t.L ? (int)(lt.sorted[p < kSegApplyMax ? p : 0] & lt.tmask) : -1;
+    return tile_blocks(g, t, my_tok, ao, bo);
+  });
+}
+
+void launch_segment_apply(const ApplyArgs& g, const int32_t* idx, const SegOut& so,
+                          unsigned grid, size_t lds, hipStream_t stream) {
+  static std::atomic<bool> lds_done{false};
+  if (lds > 64 * 1024) allow_lds(reinterpret_cast<const void*>(segment_apply_kernel), lds_done);
+  hipLaunchKernelGGL(segment_apply_kernel, dim3(grid), dim3(kNT), lds, stream, g, idx, so);
+}
+
+}  // namespace plora_impl

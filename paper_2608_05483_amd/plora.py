@@ -33,7 +33,7 @@ EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_ini
             "plora_apply_multi", "plora_workspace_bytes_multi",
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
-            "plora_pool_device_pointer",
+            "plora_pool_device_pointer", "plora_workspace_counters",
             # include/plora_attention.h
             "plora_attn_partitions", "plora_attn_workspace_bytes", "plora_attn_partial",
             "plora_attn_merge", "plora_attn_decode")
@@ -103,6 +103,8 @@ def _load() -> ctypes.CDLL:
     L.plora_debug_last_hip_error.restype = i32
     L.plora_pool_device_pointer.argtypes = [P, ctypes.POINTER(P)]
     L.plora_pool_device_pointer.restype = ctypes.c_int
+    L.plora_workspace_counters.argtypes = [P, sz, ctypes.POINTER(i64), P]
+    L.plora_workspace_counters.restype = ctypes.c_int
     L.plora_debug_set_exchange_polls.argtypes = [i32]
     L.plora_debug_set_exchange_polls.restype = None
     L.plora_attn_partitions.argtypes = [i64]
@@ -214,6 +216,14 @@ def plora_pool_device_pointer(host: int) -> int:
     return int(d.value)
 
 
+def plora_workspace_counters(ws: int, ws_bytes: int, stream: int) -> tuple:
+    """(work items that computed v alone, tokens skipped for an unusable
+    adapter entry), counted since the workspace was zeroed.  Synchronous."""
+    out = (ctypes.c_int64 * 2)()
+    _ok("plora_workspace_counters", lib.plora_workspace_counters(ws, ws_bytes, out, stream))
+    return int(out[0]), int(out[1])
+
+
 def plora_debug_set_exchange_polls(polls: int) -> None:
     lib.plora_debug_set_exchange_polls(polls)
 
@@ -323,6 +333,10 @@ class Workspace:
     def ptr(self) -> int | None:
         return self.buf.data_ptr() if self.buf is not None else None
 
+    def counters(self, stream=None) -> tuple:
+        """(exchange give-ups, skipped tokens) since the workspace was zeroed."""
+        return plora_workspace_counters(self.ptr, self.nbytes, _stream(stream))
+
 
 def segment(idx, segs: Segments, stream=None) -> None:
     plora_segment(idx.data_ptr(), segs.struct, segs.n_adapters, None, 0,
@@ -334,9 +348,11 @@ def shrink(x, ad: Adapters, segs: Segments, v, ws: Workspace, stream=None) -> No
                  v.stride(0), ws.ptr, ws.nbytes, _stream(stream))
 
 
-def expand(v, ad: Adapters, segs: Segments, y, stream=None) -> None:
+def expand(v, ad: Adapters, segs: Segments, y, stream=None, ws: Workspace | None = None) -> None:
+    """ws is optional: given, the call counts skipped tokens into it."""
     plora_expand(v.data_ptr(), v.stride(0), ad.struct, segs.struct, y.data_ptr(),
-                 y.stride(0), None, 0, _stream(stream))
+                 y.stride(0), ws.ptr if ws is not None else None,
+                 ws.nbytes if ws is not None else 0, _stream(stream))
 
 
 def apply(x, ad: Adapters, segs: Segments, y, ws: Workspace, stream=None) -> None:

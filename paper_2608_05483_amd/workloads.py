@@ -205,7 +205,7 @@ def fill_adapters(A: np.ndarray, B: np.ndarray, ranks, a_off, b_off, h_in: int,
 def make_workload(name: str, seed: int | None = None, scale: str = "paper",
                   only_used: bool = False, idx: np.ndarray | None = None,
                   n_adapters: int | None = None, h_out: int | None = None,
-                  stack_seed: int | None = None) -> Workload:
+                  stack_seed: int | None = None, ranks=None) -> Workload:
     """Build config ``name``.
 
     only_used: draw A/B only for adapters that ``idx`` references (the other
@@ -214,6 +214,8 @@ def make_workload(name: str, seed: int | None = None, scale: str = "paper",
     h_out / stack_seed: another projection of the same layer: its own output
     width and adapter stack (A/B drawn from stack_seed), with x, the ids, the
     ranks and the scales of ``seed``.
+    ranks: override the config's ranks: one int for every adapter, or an
+    int array of N entries (any values 0..128; blocks stay back to back).
     """
     c = CONFIGS[name]
     if h_out is not None:
@@ -225,7 +227,12 @@ def make_workload(name: str, seed: int | None = None, scale: str = "paper",
         idx = draw_idx(name, seed)
     idx = np.ascontiguousarray(idx, np.int32)
     T = idx.size
-    ranks = _ranks(name, seed)[:N] if N <= c.N else np.resize(_ranks(name, seed), N)
+    if ranks is not None:
+        ranks = np.array(np.broadcast_to(np.asarray(ranks, np.int32), (N,)))
+    elif N <= c.N:
+        ranks = _ranks(name, seed)[:N]
+    else:
+        ranks = np.resize(_ranks(name, seed), N)
     scales = _scales(name, seed)[:N] if N <= c.N else np.resize(_scales(name, seed), N)
     ranks = np.ascontiguousarray(ranks, np.int32)
     scales = np.ascontiguousarray(scales, np.float32)

@@ -143,12 +143,15 @@ def test_deterministic(P):
     assert all(torch.equal(outs[0], x) for x in outs[1:])
 
 
-def test_llama7b_decode_shape_sampled(P):
-    """32 heads, caches of up to 4096 keys, 8 requests: every output checked
-    against the oracle on the sampled (request, head) pairs."""
+def test_llama7b_decode_shape(P):
+    """32 heads, caches of up to 4096 keys, 8 requests (two of them full, at
+    4096 keys): every head of the two full requests and of one more, and four
+    sampled (request, head) pairs of the others, checked element-wise against
+    the oracle."""
     rng = np.random.default_rng(6)
     Bn, H, Lmax = 8, 32, 4096
     lens = rng.integers(512, Lmax + 1, Bn).astype(np.int32)
+    lens[0] = lens[3] = Lmax
     g = torch.Generator(device="cuda").manual_seed(6)
     to_bits = lambda t: t.to(torch.bfloat16).view(torch.int16)
     q = to_bits(torch.randn((Bn, H, D), device="cuda", generator=g))
@@ -161,7 +164,12 @@ def test_llama7b_decode_shape_sampled(P):
     torch.cuda.synchronize()
     ob = out.cpu().numpy().view(np.uint16)
     u16 = lambda t: t.cpu().numpy().view(np.uint16)
-    for b, h in [(0, 0), (3, 17), (7, 31), (5, 8)]:
+    for b in (0, 3, 6):
+        print(f"attention request {b}: all {H} heads, {int(lens[b])} keys", flush=True)
+        ref = OA.attention(u16(q[b:b + 1]), u16(K[b:b + 1]), u16(V[b:b + 1]), lens[b:b + 1],
+                           scale)
+        check_out(ob[b:b + 1], ref)
+    for b, h in [(1, 0), (2, 17), (7, 31), (5, 8)]:
         ref = OA.attention(u16(q[b:b + 1, h:h + 1]), u16(K[b:b + 1, h:h + 1]),
                            u16(V[b:b + 1, h:h + 1]), lens[b:b + 1], scale)
         check_out(ob[b:b + 1, h:h + 1], ref)

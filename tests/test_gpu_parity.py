@@ -262,27 +262,34 @@ def test_apply_matches_oracle(P, name, scale):
     check_y(y, yref, yout, w, strict_l2=(scale == "parity"))
 
 
-@pytest.mark.parametrize("name", ["tiny", "decode", "ragged", "prefill"])
-def test_shrink_within_bound(P, name):
-    w = workload(name, "parity")
-    say(f"shrink {name}")
-    run = Run(P, w).segment()
-    v = run.shrink().cpu().numpy()
-    vref = oracle.shrink(w.x, w.idx, w.A, w.a_off, w.ranks, w.h_in,
+def check_v_bound(w, v, idx=None):
+    """v (fp32, as the GPU wrote it) within 2 gamma_{h_in} sum_k |x_k A_kc| of
+    the oracle's v, element-wise on up to 96 sampled valid tokens; every
+    defined entry finite."""
+    idx = w.idx if idx is None else idx
+    vref = oracle.shrink(w.x, idx, w.A, w.a_off, w.ranks, w.h_in,
                          ldv=v.shape[1], n_threads=ORACLE_THREADS)
     dec = lambda b: (np.asarray(b, np.uint32) << 16).view(np.float32).astype(np.float64)
-    valid = (w.idx >= 0) & (w.idx < w.n_adapters)
+    valid = (idx >= 0) & (idx < w.n_adapters)
     tokens = np.nonzero(valid)[0]
     if tokens.size > 96:
         tokens = np.sort(np.random.default_rng(0).choice(tokens, 96, replace=False))
     for t in tokens:
-        i = int(w.idx[t])
+        i = int(idx[t])
         r = int(w.ranks[i])
         Ai = dec(w.A[w.a_off[i]:w.a_off[i] + w.h_in * r]).reshape(w.h_in, r)
         S = np.abs(dec(w.x[t])) @ np.abs(Ai)
         assert (np.abs(v[t, :r] - vref[t, :r]) <= 2 * gamma(w.h_in) * S).all(), t
     # every defined entry is finite and every token row was written
     assert np.isfinite(v[valid][:, :int(w.ranks.min())]).all()
+
+
+@pytest.mark.parametrize("name", ["tiny", "decode", "ragged", "prefill"])
+def test_shrink_within_bound(P, name):
+    w = workload(name, "parity")
+    say(f"shrink {name}")
+    run = Run(P, w).segment()
+    check_v_bound(w, run.shrink().cpu().numpy())
 
 
 @pytest.mark.parametrize("name", ["tiny", "decode", "large", "ragged", "prefill"])
@@ -435,7 +442,8 @@ def test_linear_in_scale_bitwise(P):
 
 
 def test_skipped_tokens_and_adapters(P):
-    """ids -1 / out of range, rank-0 adapters and unusable ranks keep y_base."""
+    """ids -1 / out of range and rank-0 adapters keep y_base, as the oracle
+    says; a rank that is not a multiple of 8 (12) is applied like any other."""
     w = workload("ragged", "parity")
     idx = w.idx.copy()
     idx[::5] = -1
@@ -452,23 +460,26 @@ def test_skipped_tokens_and_adapters(P):
     check_y(y, yref, yout, wr, strict_l2=True, idx=idx)
     keep = (idx < 0) | (idx >= w.n_adapters) | (idx == zero_id)
     assert (y[keep] == w.y_base[keep]).all()
-    # a rank that is not a multiple of 8 is skipped, and reported on the host
+    # a rank of 12 (stored back to back with its own row length) is the
+    # oracle's result too; the other tokens keep their bits
     ranks2 = ranks.copy()
     ranks2[bad_id] = 12
-    wb = W.Workload(**{**w.__dict__, "ranks": ranks2})
+    wb = W.make_workload("ragged", scale="parity", ranks=ranks2, idx=idx)
     rb = Run(P, wb, idx=idx).segment()
     assert P.plora_check_adapters(rb.ad.struct,
-                                  torch.cuda.current_stream().cuda_stream) == bad_id
+                                  torch.cuda.current_stream().cuda_stream) == -1
     yb = rb.apply()
+    ybr, ybo = oracle_y(wb, idx=idx)
+    check_y(yb, ybr, ybo, wb, strict_l2=True, idx=idx)
     rows = idx == bad_id
-    assert (yb[rows] == w.y_base[rows]).all()
-    assert (yb[~rows] == y[~rows]).all()
+    assert not (yb[rows] == w.y_base[rows]).all()
+    assert rb.ws.counters() == (0, 0)
 
 
 def test_check_adapters_reports_first_bad_entry(P):
     w = workload("tiny", "paper")
     ranks = w.ranks.copy()
-    ranks[2] = 12
+    ranks[2] = 24                              # above max_rank = 16
     ad = P.Adapters.from_arrays(w.A, w.B, w.a_off, w.b_off, ranks, w.scales, w.h_in,
                                 w.h_out, max_rank=16)
     s = torch.cuda.current_stream().cuda_stream
@@ -590,6 +601,11 @@ def test_adapters_read_from_a_pinned_host_pool(P):
             vv = v.cpu().numpy()
             assert np.array_equal(np.isnan(vv), np.isnan(v_dev))
             assert (vv[~np.isnan(vv)] == v_dev[~np.isnan(v_dev)]).all()
+            # and against the oracle itself, independently of the HBM run
+            yref, yout = oracle_y(w)
+            check_y(bits16(y)[:, :w.h_out], yref, yout, w, strict_l2=True)
+            check_v_bound(w, vv)
+            assert run.ws.counters() == (0, 0)
 
 
 def test_pool_pointer_must_be_pinned(P):

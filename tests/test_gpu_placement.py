@@ -1,8 +1,8 @@
 """The placement decision driving the kernels (strategies E1 / E2): over a
 sequence of decode batches, an HBM budget of a fraction of the adapter bytes,
 adapters cached by the selection and the rest read from a pinned host pool.
-Every step's y must be the all-HBM result bit for bit (the same kernels read
-the same values, wherever they live)."""
+Every step's y must meet the oracle's bars, and be the all-HBM result bit for
+bit (the same kernels read the same values, wherever they live)."""
 import numpy as np
 import pytest
 
@@ -12,6 +12,7 @@ torch = pytest.importorskip("torch")
 
 from paper_2608_05483_amd import placement as PL  # noqa: E402
 from paper_2608_05483_amd import workloads as W  # noqa: E402
+from test_gpu_parity import check_y, oracle_y  # noqa: E402
 
 
 @pytest.fixture(scope="module")
@@ -60,6 +61,9 @@ def test_placed_adapters_give_the_all_hbm_result(P, budget_frac):
         P.segment_apply(idx_d, x, ad, segs_p, y_p, ws)
         P.segment_apply(idx_d, x, full, segs_f, y_f, ws)
         torch.cuda.synchronize()
+        wk = W.with_idx(w, idx)
+        yref, yout = oracle_y(wk)
+        check_y(bits16(y_p), yref, yout, wk, strict_l2=True)
         assert (bits16(y_p) == bits16(y_f)).all(), step
         served = Bc > 0
         n_e1 += int((served & d.resident).sum())
@@ -69,3 +73,4 @@ def test_placed_adapters_give_the_all_hbm_result(P, budget_frac):
         temp.step()
     if budget_frac >= 0.2:
         assert n_e1 > 0      # the hot adapters were served from HBM
+    assert ws.counters() == (0, 0)

@@ -255,14 +255,16 @@ def _exact_apply(c, t):
                                for cc in range(r)) for j in range(h_out)]
 
 
-@pytest.mark.parametrize("seed", [0, 1, 2])
-def test_apply_exact_on_small_integers(seed):
+@pytest.mark.parametrize("seed,ranks", [(0, [8, 16, 0]), (1, [8, 16, 0]), (2, [8, 16, 0]),
+                                        (3, [1, 3, 12, 0, 5]), (4, [2, 24, 7, 4, 13])])
+def test_apply_exact_on_small_integers(seed, ranks):
     """Integer inputs keep every fp32 partial sum exact (< 2^24), so the
     oracle must reproduce the pure-Python exact result bit for bit, and its
-    bf16 output must be the exact result rounded to nearest-even."""
+    bf16 output must be the exact result rounded to nearest-even.  The ranks
+    include ones that are not multiples of 8 (rows of A_i of odd length)."""
     rng = np.random.default_rng(seed)
-    c = _int_case(rng, T=7, N=3, h_in=24, h_out=16, ranks=[8, 16, 0],
-                  scales=[1.0, 0.5, 2.0])
+    c = _int_case(rng, T=7, N=len(ranks), h_in=24, h_out=16, ranks=ranks,
+                  scales=[1.0, 0.5, 2.0, 0.25, 4.0][:len(ranks)])
     yref, yout = oracle.apply(c["x"], c["idx"], c["A"], c["a_off"], c["B"],
                               c["b_off"], c["ranks"], c["scales"], c["y"],
                               c["h_in"], c["h_out"])
