@@ -288,6 +288,25 @@ plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t 
                                  uint16_t* y, int64_t ldy, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
+/*
+ * plora_segment_apply for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same call without a workspace argument.  Its workspace is
+ * a static device array of the library, 65 MiB on every GPU it runs on, held
+ * until the process ends, zero when the library is loaded and then carrying
+ * the exchange's epochs from call to call.  Batches of at most 256 tokens;
+ * a larger T returns PLORA_ERR_UNSUPPORTED before anything is launched.
+ * Allocates nothing and keeps no pointer; results are the bits
+ * plora_segment_apply gives with a workspace of its own.  Every call on one
+ * GPU shares that GPU's array: calls that overlap in time on one GPU (other
+ * streams, other threads) race and must be ordered by the caller.  Other
+ * arguments and errors as for plora_segment_apply; PLORA_ERR_HIP also if the
+ * array's device address cannot be found.
+ */
+plora_status plora_segment_apply_noalloc(const int32_t* idx, const uint16_t* x, int64_t ldx,
+                                         const plora_adapters* ad, const plora_segments* seg,
+                                         uint16_t* y, int64_t ldy, hipStream_t stream);
+
 /* Host.  How many launches plora_segment_apply makes for a batch of T
  * tokens over this stack: 1 (the one-launch form), 2 (plora_segment then
  * a one-launch plora_apply) or 3 (then a two-launch one); 0 for T <= 0 or

@@ -17,6 +17,8 @@
 //                  apply kernels below.
 #include "plora_dev.h"
 
+#include <mutex>
+
 namespace plora_impl {
 namespace {
 // ---------------------------------------------------------------------------
@@ -120,7 +122,7 @@ struct WsLayout {
 
 constexpr int kCounters = 2;   // workspace counters after the epochs (see ApplyArgs)
 
-inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+constexpr size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // n adapter stacks (the projections of plora_apply_multi; n = 1 otherwise)
 // sharing the batch: n cap8 tile slots, and the largest partial-sum section.
@@ -270,6 +272,58 @@ plora_status launch_items(ItemLauncher launch, const ApplyArgs& g, int s_max,
   return launch_status();
 }
 
+// ---------------------------------------------------------------------------
+// the allocation-free entry point's scratch
+// ---------------------------------------------------------------------------
+
+// Largest batch plora_segment_apply_noalloc takes, and the workspace such a
+// batch needs at most: the exchange regions of min(kXSlots, cap8) tile
+// slots (cap8 <= kNoAllocTokens) and the partial sums of v for up to 8
+// slices of h_in at rank 128, after the epochs and counters.
+constexpr int32_t kNoAllocTokens = 256;
+constexpr size_t kScratchBytes =
+    align256(align256(align256((size_t)(kXSlots + kCounters) * sizeof(uint64_t)) +
+                      (size_t)std::min(kXSlots, kNoAllocTokens) * kSlotWords * sizeof(uint64_t)) +
+             (size_t)8 * kNoAllocTokens * PLORA_MAX_RANK * sizeof(float));
+
+// The device address of `scratch` on the current device, looked up once per
+// device with that device current (each device holds its own copy of the
+// array at its own address); null if the lookup fails.
+void* scratch_for_device();
+
+}  // namespace
+}  // namespace plora_impl
+
+// The workspace of plora_segment_apply_noalloc: one per device, zero from
+// the module's load, then carrying the exchange's epochs from call to call as
+// any workspace does.  Host code never uses this name as an address (it is a
+// host-side stand-in); it takes the pointer scratch_for_device() returns.
+static __device__ __align__(256) unsigned char scratch[plora_impl::kScratchBytes];
+
+namespace plora_impl {
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];
+
+void* scratch_for_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
 }  // namespace
 }  // namespace plora_impl
 
@@ -372,6 +426,28 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   st = launch_items(launch_shrink_part, gs, g.ks_max, stream);
   if (st != PLORA_OK) return st;
   return launch_items(launch_expand_parts, g, g.js_max, stream);
+}
+
+plora_status plora_segment_apply_noalloc(const int32_t* idx, const uint16_t* x, int64_t ldx,
+                                         const plora_adapters* ad, const plora_segments* seg,
+                                         uint16_t* y, int64_t ldy, hipStream_t stream) {
+  if (!ad || !seg) return PLORA_ERR_INVALID_ARG;
+  plora_status st = check_adapters_host(ad);
+  if (st != PLORA_OK) return st;
+  st = check_segments_host(seg, ad->n_adapters);
+  if (st != PLORA_OK) return st;
+  if (seg->T > kNoAllocTokens) return PLORA_ERR_UNSUPPORTED;
+  if (seg->T == 0) return PLORA_OK;
+  if (!idx || !x || !y) return PLORA_ERR_INVALID_ARG;
+  if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
+  if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
+  if (ws_layout(seg->T, ad).total > kScratchBytes) return PLORA_ERR_UNSUPPORTED;
+  void* ws = scratch_for_device();
+  if (!ws) {
+    g_last_hip_error.store((int32_t)hipErrorInvalidSymbol);
+    return PLORA_ERR_HIP;
+  }
+  return plora_segment_apply(idx, x, ldx, ad, seg, y, ldy, ws, kScratchBytes, stream);
 }
 
 int32_t plora_segment_apply_launches(int32_t T, const plora_adapters* ad) {

@@ -34,6 +34,7 @@ EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_ini
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
             "plora_pool_device_pointer", "plora_workspace_counters",
+            "plora_segment_apply_noalloc",
             # include/plora_attention.h
             "plora_attn_partitions", "plora_attn_workspace_bytes", "plora_attn_partial",
             "plora_attn_merge", "plora_attn_decode")
@@ -90,6 +91,8 @@ def _load() -> ctypes.CDLL:
     L.plora_expand.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_apply.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_segment_apply.argtypes = [P, P, i64, AD, SG, P, i64, P, sz, P]
+    L.plora_segment_apply_noalloc.argtypes = [P, P, i64, AD, SG, P, i64, P]
+    L.plora_segment_apply_noalloc.restype = ctypes.c_int
     L.plora_segment_apply_launches.argtypes = [i32, AD]
     L.plora_segment_apply_launches.restype = i32
     L.plora_apply_multi.argtypes = [P, i64, AD, i32, SG, ctypes.POINTER(P),
@@ -180,6 +183,13 @@ def plora_segment_apply(idx: int, x: int, ldx: int, ad: plora_adapters, seg: plo
     _ok("plora_segment_apply",
         lib.plora_segment_apply(idx, x, ldx, ctypes.byref(ad), ctypes.byref(seg), y, ldy, ws,
                                 ws_bytes, stream))
+
+
+def plora_segment_apply_noalloc(idx: int, x: int, ldx: int, ad: plora_adapters,
+                                seg: plora_segments, y: int, ldy: int, stream: int) -> None:
+    _ok("plora_segment_apply_noalloc",
+        lib.plora_segment_apply_noalloc(idx, x, ldx, ctypes.byref(ad), ctypes.byref(seg), y,
+                                        ldy, stream))
 
 
 def plora_segment_apply_launches(T: int, ad: plora_adapters) -> int:
@@ -364,6 +374,13 @@ def segment_apply(idx, x, ad: Adapters, segs: Segments, y, ws: Workspace, stream
     """segment() then apply() on the same batch, as one call."""
     plora_segment_apply(idx.data_ptr(), x.data_ptr(), x.stride(0), ad.struct, segs.struct,
                         y.data_ptr(), y.stride(0), ws.ptr, ws.nbytes, _stream(stream))
+
+
+def segment_apply_noalloc(idx, x, ad: Adapters, segs: Segments, y, stream=None) -> None:
+    """segment_apply() without a workspace: the library's static one (at
+    most 256 tokens; calls on one GPU must not overlap)."""
+    plora_segment_apply_noalloc(idx.data_ptr(), x.data_ptr(), x.stride(0), ad.struct,
+                                segs.struct, y.data_ptr(), y.stride(0), _stream(stream))
 
 
 # ---- split-KV decode attention (include/plora_attention.h) --------------------

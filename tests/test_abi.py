@@ -285,6 +285,32 @@ def test_segment_apply_host_checks():
     assert _segapply_status(seg=empty, idx=None, x=None, y=None) == P.PLORA_OK
 
 
+def test_segment_apply_noalloc_host_checks():
+    """The allocation-free call refuses batches above its static workspace's
+    256 tokens, and checks its arguments like plora_segment_apply, before
+    anything touches the device."""
+    L = P.lib
+
+    def st(ad=None, seg=None, idx=FAKE, x=FAKE, ldx=256, y=FAKE, ldy=256):
+        ad = ad or _ad()
+        seg = seg or _seg()
+        return L.plora_segment_apply_noalloc(idx, x, ldx, ctypes.byref(ad), ctypes.byref(seg),
+                                             y, ldy, None)
+    dec = _ad(n_adapters=1000, h_in=4096, h_out=4096, max_rank=128)
+    assert st(ad=dec, seg=_seg(T=257, N=1000), ldx=4096, ldy=4096) == P.PLORA_ERR_UNSUPPORTED
+    assert st(ad=dec, seg=_seg(T=16384, N=1000), ldx=4096, ldy=4096) == \
+        P.PLORA_ERR_UNSUPPORTED
+    assert st(idx=None) == P.PLORA_ERR_INVALID_ARG
+    assert st(x=None) == P.PLORA_ERR_INVALID_ARG
+    assert st(ldx=200) == P.PLORA_ERR_INVALID_ARG
+    assert st(ldy=260) == P.PLORA_ERR_UNSUPPORTED
+    assert st(y=FAKE + 8) == P.PLORA_ERR_UNSUPPORTED
+    assert st(ad=_ad(max_rank=136)) == P.PLORA_ERR_UNSUPPORTED
+    assert st(seg=_seg(cap=3)) == P.PLORA_ERR_INVALID_ARG
+    empty = _seg(T=0, N=4, perm=None, seg_ptr=None, seg_id=None, meta=None, tiles=None)
+    assert st(seg=empty, idx=None, x=None, y=None) == P.PLORA_OK
+
+
 def test_adapter_blocks_must_stay_below_2gib():
     # adapter blocks are read through 32-bit byte offsets: max(h_in, h_out)
     # * max_rank * 2 bytes must stay below 2^31 (checked before the empty
