@@ -4,29 +4,36 @@
 One step = one pass of the whole hot path over one batch already resident in
 HBM: plora_segment_apply, which groups the batch's tokens by adapter (the
 plora_segment outputs) and applies y += s_i (x A_i) B_i for every token.  For
-decode-sized batches that is one launch; larger batches take plora_segment
-then plora_apply.  With --projections > 1 a step is plora_segment then one
-plora_apply_multi.  Each step takes a fresh token-to-adapter draw from a pool
-drawn up front, and a different replica of the adapter stack, so that an
-adapter's bytes are never still sitting in the 256 MB Infinity Cache from an
-earlier step (a served model revisits one projection's stack only after every
-other LoRA projection of every layer).
+batches of up to 256 tokens that is one launch; larger batches take
+plora_segment then plora_apply.  With --projections > 1 a step is
+plora_segment then one plora_apply_multi.  Each step takes a fresh
+token-to-adapter draw from a pool drawn up front, a different replica of the
+adapter stack and a different replica of the activations, so that neither an
+adapter's bytes nor x and y are still sitting in the 256 MB Infinity Cache
+from an earlier step (a served model revisits one projection's stack only
+after every other LoRA projection of every layer).
 
-Prints ONE JSON line.  ``value`` is whole-job tokens/s over the timed steps
-(wall clock), the K steps launched as one captured HIP graph (``--eager``:
-one launch per call from Python; the eager time is reported too).
+Prints ONE JSON line.  The top level is the headline configuration (--config,
+the 1000-adapter Llama-7B-shaped decode batch by default); ``configs`` holds
+the same measurements for the other workloads (large decode batch, ragged
+ranks, prefill + decode), taken in the same run.  ``value`` is whole-job
+tokens/s over the timed steps (wall clock), the K steps launched as one
+captured HIP graph (``--eager``: one launch per call from Python).
 ``roofline`` prices the dominant kernel: algorithmic bytes per step
 (distinct adapters' A_i and B_i, 2 r_i (h_in + h_out) bytes each, plus x
 read, y read and written, and the token ids) over that kernel's average
 duration.  Where a step is one launch, that is the step graph's duration
 between two HIP events recorded on the stream the kernels run on; otherwise
 it is the apply's: K plora_apply calls captured as one graph and replayed
-between two such events.  ``cpu_baseline`` times the CPU oracle on a bounded
-sample of the same workload.
+between two such events.  ``read_ceiling`` is a plain 128-bit read of exactly
+the adapter blocks each step touches, timed the same way (K launches in one
+graph).  ``cpu_baseline`` times the CPU oracle on a bounded sample of the
+headline workload.
 """
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import math
@@ -39,8 +46,9 @@ import numpy as np
 HBM_PEAK_GBPS = 8000.0
 MALL_BYTES = 256 << 20
 ROOT = os.path.dirname(os.path.abspath(__file__))
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_05483_amd", "csrc", "plora.hip")
+CSRC = os.path.join(ROOT, "paper_2608_05483_amd", "csrc")
 PROFILES = os.path.join(ROOT, "profiles")
+EXTRA_DEFAULT = ("large", "ragged", "prefill")
 
 
 def parse():
@@ -49,7 +57,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="decode",
-                    choices=["tiny", "decode", "large", "ragged", "prefill"])
+                    choices=["tiny", "decode", "large", "ragged", "prefill"],
+                    help="the headline workload (top level of the JSON line)")
+    ap.add_argument("--also", default="auto",
+                    help="comma-separated workloads also measured in this run and reported "
+                         "under 'configs' ('auto': large, ragged and prefill next to the "
+                         "decode headline, none otherwise; 'none')")
     ap.add_argument("--draws", type=int, default=64,
                     help="distinct token-to-adapter draws cycled through")
     ap.add_argument("--replicas", type=int, default=0,
@@ -75,15 +88,24 @@ def parse():
     return ap.parse_args()
 
 
+def kernel_sources():
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.h")))
+
+
 def source_digest() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """sha256 over every kernel source file (names and contents)."""
+    h = hashlib.sha256()
+    for path in kernel_sources():
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic(stem: str):
     """HBM bytes per launch of the priced kernel from the committed counter
     summary (profiles/<stem>_traffic.txt, stem = kernel and workload), or
-    None when there is none or the kernel source has changed since the
+    None when there is none or the kernel sources have changed since the
     counters were taken."""
     path = os.path.join(PROFILES, f"{stem}_traffic.txt")
     if not os.path.exists(path):
@@ -126,6 +148,255 @@ def describe(name, c):
             f"N={c.N} bf16 adapters, ids {dist}")
 
 
+def graph_seconds(torch, calls, K, eager=False, wall=None):
+    """K calls (calls(k) enqueues call k) captured as one HIP graph, replayed
+    once untimed and once between two events recorded on the stream it is
+    replayed on; seconds for the K calls.  eager: the K calls issued from
+    Python instead (which floors at the host's launch rate).  wall, a list,
+    receives the host's wall-clock seconds of the timed pass, from a
+    synchronized device to a synchronized device."""
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g = None
+    if not eager:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for k in range(K):
+                calls(k)
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record()
+    if eager:
+        for k in range(K):
+            calls(k)
+    else:
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    if wall is not None:
+        wall.append(time.perf_counter() - t0)
+    return e0.elapsed_time(e1) / 1e3
+
+
+class ReadProbe:
+    """The same-footprint plain-read ceiling (csrc/read_ceiling.hip)."""
+
+    def __init__(self, torch, dev, draws, N):
+        import ctypes
+        from paper_2608_05483_amd import build as B
+        self.torch = torch
+        pl = ctypes.CDLL(B.PROBE_LIB)
+        pl.plora_probe_read.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int32] * 3 + \
+            [ctypes.c_void_p] * 2
+        pl.plora_probe_sink_words.argtypes = [ctypes.c_int32]
+        self.pl = pl
+        self.uniq = [torch.from_numpy(np.unique(d[(d >= 0) & (d < N)]).astype(np.int32)).to(dev)
+                     for d in draws]
+        self.sink = torch.empty(pl.plora_probe_sink_words(max(1, max(u.numel()
+                                                                     for u in self.uniq))),
+                                dtype=torch.int32, device=dev)
+
+    def read(self, ad, d, h_in, h_out):
+        # the stream is looked up at call time, so that a call made under graph
+        # capture is captured
+        rc = self.pl.plora_probe_read(ad.A.data_ptr(), ad.B.data_ptr(), ad.a_off.data_ptr(),
+                                      ad.b_off.data_ptr(), ad.ranks.data_ptr(),
+                                      self.uniq[d].data_ptr(), self.uniq[d].numel(), h_in, h_out,
+                                      self.sink.data_ptr(),
+                                      self.torch.cuda.current_stream().cuda_stream)
+        assert rc == 0
+
+
+class ApplyBench:
+    """One workload on the device: adapter-stack replicas, activation
+    replicas, a pool of token draws and their segmentations."""
+
+    def __init__(self, torch, P, W, dev, name, args, n_proj=1):
+        self.torch, self.P, self.W, self.dev, self.name = torch, P, W, dev, name
+        self.args = args
+        c = W.CONFIGS[name]
+        self.c = c
+        seed = 1000 + W.CONFIG_NAMES.index(name)
+        w = W.make_workload(name)
+        self.w = w
+        N = self.N = w.n_adapters
+        self.n_proj = n_proj
+        wps = [w] if n_proj == 1 else W.make_projections(name, n_proj=n_proj)
+        if len(wps) != n_proj:
+            print(f"bench.py: config {name} defines {len(wps)} projections", file=sys.stderr)
+            sys.exit(2)
+        self.wps = wps
+        draws = [W.draw_idx(name, seed, d) for d in range(args.draws)]
+        self.draws = draws
+        Tmax = self.Tmax = max(d.size for d in draws)
+        self.act_bytes = lambda T: T * (2 * w.h_in + sum(4 * wp.h_out for wp in wps)) + 4 * T
+        self.ad_bytes = [sum(W.adapter_bytes(wp.ranks, d, wp.h_in, wp.h_out, N) for wp in wps)
+                         for d in draws]
+        self.tot_bytes = [a + self.act_bytes(d.size) for a, d in zip(self.ad_bytes, draws)]
+
+        bases = [P.Adapters.from_workload(wp, device=dev) for wp in wps]
+        self.bases = bases
+        stack_bytes = sum(2 * (b.A.numel() + b.B.numel()) for b in bases)
+        R = args.replicas
+        if R <= 0:
+            per_step = max(1, int(np.mean(self.ad_bytes)))
+            R = max(2, min(64, math.ceil(3 * MALL_BYTES / per_step)))
+            R = max(1, min(R, int((96 << 30) // max(stack_bytes, 1))))
+        self.R = R
+        self.reps = [bases]
+        for _ in range(R - 1):
+            self.reps.append([P.Adapters(b.A.clone(), b.B.clone(), b.a_off, b.b_off, b.ranks,
+                                         b.scales, b.h_in, b.h_out, b.max_rank) for b in bases])
+        # activation replicas: enough that x and y of earlier steps have left
+        # the Infinity Cache too
+        act_step = max(1, int(np.mean([self.act_bytes(d.size) for d in draws])))
+        RA = max(1, min(64, math.ceil(3 * MALL_BYTES / act_step)))
+        self.RA = RA
+        xw = w if Tmax == w.T else W.with_idx(w, np.zeros(Tmax, np.int32))
+        x0 = torch.from_numpy(xw.x).view(torch.int16).to(dev)
+        self.xs = [x0] + [x0.clone() for _ in range(RA - 1)]
+        self.ys = []                        # [projection][activation replica]
+        for wp in wps:
+            y_host = np.zeros((Tmax, wp.h_out), np.uint16)
+            n = min(Tmax, wp.T)
+            y_host[:n] = wp.y_base[:n]
+            y0 = torch.from_numpy(y_host).view(torch.int16).to(dev)
+            self.ys.append([y0] + [y0.clone() for _ in range(RA - 1)])
+        self.ws = P.Workspace(Tmax, bases if n_proj > 1 else bases[0])
+        self.idx_dev = [torch.from_numpy(d).to(dev) for d in draws]
+        self.segs = [P.Segments(d.size, N, device=dev) for d in draws]
+        self.apply_call = self._apply_call
+
+    def _apply_call(self, k, separate=False):
+        P = self.P
+        d = k % len(self.draws)
+        T = self.draws[d].size
+        rp = self.reps[k % self.R]
+        a = k % self.RA
+        x = self.xs[a][:T]
+        if self.n_proj == 1:
+            P.apply(x, rp[0], self.segs[d], self.ys[0][a][:T], self.ws)
+        elif separate:
+            for q in range(self.n_proj):
+                P.apply(x, rp[q], self.segs[d], self.ys[q][a][:T], self.ws)
+        else:
+            P.apply_multi(x, rp, self.segs[d], [yq[a][:T] for yq in self.ys], self.ws)
+
+    def step(self, k, ev=None):
+        P = self.P
+        d = k % len(self.draws)
+        if ev is not None:
+            ev[0].record()
+        if self.n_proj == 1:
+            # segmentation and apply in one call (one launch for batches of up to
+            # 256 tokens; plora_segment then plora_apply otherwise)
+            T = self.draws[d].size
+            a = k % self.RA
+            P.segment_apply(self.idx_dev[d], self.xs[a][:T], self.reps[k % self.R][0],
+                            self.segs[d], self.ys[0][a][:T], self.ws)
+        else:
+            P.segment(self.idx_dev[d], self.segs[d])
+            self.apply_call(k)
+        if ev is not None:
+            ev[1].record()
+
+    def one_launch(self):
+        return self.n_proj == 1 and all(
+            self.P.plora_segment_apply_launches(d.size, self.bases[0].struct) == 1
+            for d in self.draws)
+
+    def measure(self, K, warmup, eager=False, isolated=False, warm=False, ceiling=True):
+        torch, P, args = self.torch, self.P, self.args
+        for k in range(warmup):
+            self.step(k)
+        torch.cuda.synchronize()
+        out = {}
+        # eager steps with events around each (only where asked: the host
+        # floors each such step at its launch rate)
+        if isolated:
+            evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(K)]
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for k in range(K):
+                self.step(warmup + k, evs[k])
+            torch.cuda.synchronize()
+            out["wall_eager"] = time.perf_counter() - t0
+            ms = np.array([a.elapsed_time(b) for a, b in evs])
+            out["isolated_us"] = {"mean": round(float(ms.mean()) * 1e3, 3),
+                                  "p10": round(float(np.percentile(ms, 10)) * 1e3, 3),
+                                  "p90": round(float(np.percentile(ms, 90)) * 1e3, 3)}
+        # the K steps as one graph (or eager): wall clock and events
+        wall = []
+        step_s = graph_seconds(torch, lambda k: self.step(warmup + k), K, eager, wall)
+        out["wall"] = wall[0]
+        out["step_s"] = step_s
+        ks = [(warmup + k) % len(self.draws) for k in range(K)]
+        out["tokens"] = sum(self.draws[d].size for d in ks)
+        out["bytes_total"] = sum(self.tot_bytes[d] for d in ks)
+        out["bytes_adapter"] = sum(self.ad_bytes[d] for d in ks)
+        # the apply's own duration: the same draws, stacks and activations,
+        # segments made beforehand
+        for d in range(len(self.draws)):
+            P.segment(self.idx_dev[d], self.segs[d])
+        torch.cuda.synchronize()
+        out["apply_s"] = graph_seconds(torch, lambda k: self.apply_call(warmup + k), K, eager)
+        if warm and self.n_proj == 1 and self.R > 1:
+            # one stack replica and one activation replica: the adapters stay in
+            # the Infinity Cache from call to call (reported, never priced)
+            R, RA = self.R, self.RA
+            self.R, self.RA = 1, 1
+            out["warm_s"] = graph_seconds(torch, lambda k: self.apply_call(warmup + k), K, eager)
+            self.R, self.RA = R, RA
+        if self.n_proj > 1:
+            out["separate_s"] = graph_seconds(
+                torch, lambda k: self.apply_call(warmup + k, True), K, eager)
+        if ceiling and self.n_proj == 1:
+            probe = ReadProbe(torch, self.dev, self.draws, self.N)
+            w = self.w
+            rd = lambda k: probe.read(self.reps[(warmup + k) % self.R][0],
+                                      (warmup + k) % len(self.draws), w.h_in, w.h_out)
+            for k in range(warmup):
+                rd(k)
+            out["read_s"] = graph_seconds(torch, rd, K, eager)
+        one = self.one_launch() and not eager
+        out["one_launch"] = one
+        out["priced_s"] = step_s if one else out["apply_s"]
+        out["kernel"] = ("segment_apply_kernel (plora_segment_apply)" if one else
+                         "plora_apply" if self.n_proj == 1 else "plora_apply_multi")
+        stem = ("plora_segment_apply_" if one else "plora_apply_") + self.name
+        out["traffic"] = measured_traffic(stem) if self.n_proj == 1 else None
+        return out
+
+
+def summary(b, m, K):
+    """The per-workload record of the 'configs' object."""
+    bt = m["bytes_total"] / K
+    achieved = m["bytes_total"] / m["priced_s"] / 1e9
+    rec = {
+        "workload": describe(b.name, b.c),
+        "tokens_per_step": round(m["tokens"] / K, 1),
+        "tokens_per_s": round(m["tokens"] / m["wall"], 1),
+        "step_us": round(m["step_s"] / K * 1e6, 3),
+        "kernel": m["kernel"],
+        "us_per_launch": round(m["priced_s"] / K * 1e6, 3),
+        "bytes_per_launch": int(bt),
+        "adapter_bytes_per_launch": int(m["bytes_adapter"] / K),
+        "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": m["traffic"],
+        "traffic_over_algorithmic": (None if m["traffic"] is None
+                                     else round(m["traffic"] / bt, 3)),
+        "apply_us": round(m["apply_s"] / K * 1e6, 3),
+        "adapter_GBps": round(m["bytes_adapter"] / m["apply_s"] / 1e9, 1),
+        "stack_replicas": b.R, "activation_replicas": b.RA,
+    }
+    if "read_s" in m:
+        rec["read_ceiling_us"] = round(m["read_s"] / K * 1e6, 3)
+        rec["read_ceiling_frac"] = round(m["bytes_adapter"] / m["read_s"] / 1e9 /
+                                         HBM_PEAK_GBPS, 4)
+    return rec
+
+
 def bench_attention(args):
     """plora_attn_decode on 64 requests x 32 heads x head dim 128 with caches
     of U{512..4096} keys (seeded), one HBM-resident bf16 KV cache per step
@@ -155,20 +426,9 @@ def bench_attention(args):
         step(k)
     torch.cuda.synchronize()
     Ks = args.steps
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for k in range(Ks):
-            step(k)
-    graph.replay()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    e0.record()
-    graph.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ev = e0.elapsed_time(e1) / 1e3
+    walls = []
+    ev = graph_seconds(torch, step, Ks, wall=walls)
+    wall = walls[0]
     kv_bytes = int(lens_np.sum()) * H * D * 2 * 2
     step_bytes = kv_bytes + 2 * Bn * H * D * 2
     achieved = step_bytes / (ev / Ks) / 1e9
@@ -209,6 +469,92 @@ def bench_attention(args):
         "cpu_baseline": cpu}), flush=True)
 
 
+def placement_split(torch, P, b, args, K):
+    """The apply with adapters K.. read from the pinned host pool (E2) and
+    the rest from HBM (E1), next to the cost model's prediction."""
+    from paper_2608_05483_amd import placement as PL
+    w, N, dev = b.w, b.N, b.dev
+    Kp = args.pool_from
+    A_pool = torch.from_numpy(w.A.view(np.int16)).pin_memory()
+    B_pool = torch.from_numpy(w.B.view(np.int16)).pin_memory()
+    in_pool = np.arange(N) >= Kp
+    a_off = torch.from_numpy(np.where(in_pool, -1 - w.a_off, w.a_off).astype(np.int64)).to(dev)
+    b_off = torch.from_numpy(np.where(in_pool, -1 - w.b_off, w.b_off).astype(np.int64)).to(dev)
+    pool_reps = [P.Adapters(rp[0].A, rp[0].B, a_off, b_off, rp[0].ranks, rp[0].scales,
+                            w.h_in, w.h_out, w.max_rank, A_pool=A_pool, B_pool=B_pool)
+                 for rp in b.reps]
+
+    def pool_call(k):
+        d = k % len(b.draws)
+        T = b.draws[d].size
+        a = k % b.RA
+        P.apply(b.xs[a][:T], pool_reps[k % b.R], b.segs[d], b.ys[0][a][:T], b.ws)
+
+    pool_s = graph_seconds(torch, lambda k: pool_call(args.warmup + k), K, args.eager)
+    apply_s = graph_seconds(torch, lambda k: b.apply_call(args.warmup + k), K, args.eager)
+    hw = PL.Hardware()
+    model_split, model_hbm, pool_bytes = [], [], []
+    for d in b.draws:
+        ok = (d >= 0) & (d < N)
+        Bc = np.bincount(d[ok], minlength=N)
+        st = np.where(in_pool, PL.E2, PL.E1).astype(object)
+        model_split.append(PL.lora_time(Bc, w.ranks, st, w.h_in, w.h_out, hw))
+        model_hbm.append(PL.lora_time(Bc, w.ranks, np.full(N, PL.E1, dtype=object),
+                                      w.h_in, w.h_out, hw))
+        pool_bytes.append(sum(PL.adapter_bytes(w.ranks[a], w.h_in, w.h_out)
+                              for a in np.unique(d[ok]) if a >= Kp))
+    return {
+        "pool_from": Kp,
+        "apply_us_split": round(pool_s / K * 1e6, 3),
+        "apply_us_all_hbm": round(apply_s / K * 1e6, 3),
+        "pool_bytes_per_call": int(np.mean(pool_bytes)),
+        "model_us_split": round(float(np.mean(model_split)) * 1e6, 3),
+        "model_us_all_hbm": round(float(np.mean(model_hbm)) * 1e6, 3),
+        "model_hardware": {"C_gpu": hw.C_gpu, "W_gpu": hw.W_gpu, "W_link": hw.W_link,
+                           "L_link": hw.L_link},
+    }
+
+
+def cpu_baseline(W, b, args):
+    """The CPU oracle, as it stands, on a bounded sample of the workload."""
+    sys.path.insert(0, ROOT)
+    import oracle
+    w, wps, draws = b.w, b.wps, b.draws
+    cores = len(os.sched_getaffinity(0))
+
+    def run(seconds, threads):
+        n_done, toks, t_cpu = 0, 0, 0.0
+        while t_cpu < seconds:
+            d = draws[n_done % len(draws)]
+            wd = w if d.size == w.T else W.with_idx(w, d)
+            t1 = time.perf_counter()
+            for wp in wps:
+                oracle.apply(wd.x, d, wp.A, wp.a_off, wp.B, wp.b_off, wp.ranks, wp.scales,
+                             np.zeros((d.size, wp.h_out), np.uint16), w.h_in, wp.h_out,
+                             n_threads=threads)
+            t_cpu += time.perf_counter() - t1
+            toks += d.size
+            n_done += 1
+        return n_done, toks, t_cpu
+
+    n_done, toks, t_cpu = run(args.cpu_seconds, cores)
+    k1, toks1, t1_cpu = run(args.cpu_seconds / 10, 1)
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(toks / t_cpu, 1), "unit": "tokens/s", "cores": cores,
+            "kind": "oracle", "value_1_thread": round(toks1 / t1_cpu, 1), "cpu_model": model,
+            "sample": f"{n_done} batches of this workload, cycling its "
+                      f"{len(draws)} token draws ({toks} tokens, {t_cpu:.1f} s), "
+                      f"fp32 C oracle, OpenMP over tokens on {cores} threads; "
+                      f"one thread: {k1} batches ({toks1} tokens, {t1_cpu:.1f} s)"}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -231,354 +577,86 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     name = args.config
-    c = W.CONFIGS[name]
-    seed = 1000 + W.CONFIG_NAMES.index(name)
-    w = W.make_workload(name)
-    N = w.n_adapters
-    n_proj = args.projections
-    # the projections of one layer that share x (projection 0 is the config's
-    # own workload); one projection is the plain plora_apply
-    wps = [w] if n_proj == 1 else W.make_projections(name, n_proj=n_proj)
-    if len(wps) != n_proj:
-        print(f"bench.py: config {name} defines {len(wps)} projections", file=sys.stderr)
-        sys.exit(2)
-
-    # ---- token-to-adapter draws -------------------------------------------------
-    draws = [W.draw_idx(name, seed, d) for d in range(args.draws)]
-    Tmax = max(d.size for d in draws)
-    act_bytes = lambda T: T * (2 * w.h_in + sum(4 * wp.h_out for wp in wps)) + 4 * T
-    ad_bytes = [sum(W.adapter_bytes(wp.ranks, d, wp.h_in, wp.h_out, N) for wp in wps)
-                for d in draws]
-    tot_bytes = [a + act_bytes(d.size) for a, d in zip(ad_bytes, draws)]
-
-    # ---- device buffers -----------------------------------------------------------
-    bases = [P.Adapters.from_workload(wp, device=dev) for wp in wps]
-    stack_bytes = sum(2 * (b.A.numel() + b.B.numel()) for b in bases)
-    R = args.replicas
-    if R <= 0:
-        per_step = max(1, int(np.mean(ad_bytes)))
-        R = max(2, min(64, math.ceil(3 * MALL_BYTES / per_step)))
-        R = max(1, min(R, int((96 << 30) // max(stack_bytes, 1))))
-    reps = [bases]
-    for _ in range(R - 1):
-        reps.append([P.Adapters(b.A.clone(), b.B.clone(), b.a_off, b.b_off, b.ranks, b.scales,
-                                b.h_in, b.h_out, b.max_rank) for b in bases])
-    xw = w if Tmax == w.T else W.with_idx(w, np.zeros(Tmax, np.int32))
-    x = torch.from_numpy(xw.x).view(torch.int16).to(dev)
-    ys = []
-    for wp in wps:
-        y_host = np.zeros((Tmax, wp.h_out), np.uint16)
-        n = min(Tmax, wp.T)
-        y_host[:n] = wp.y_base[:n]
-        ys.append(torch.from_numpy(y_host).view(torch.int16).to(dev))
-    ws = P.Workspace(Tmax, bases if n_proj > 1 else bases[0])
-    idx_dev = [torch.from_numpy(d).to(dev) for d in draws]
-    segs = [P.Segments(d.size, N, device=dev) for d in draws]
-
-    def apply_call(k, separate=False):
-        d = k % len(draws)
-        T = draws[d].size
-        rp = reps[k % R]
-        if n_proj == 1:
-            P.apply(x[:T], rp[0], segs[d], ys[0][:T], ws)
-        elif separate:
-            for q in range(n_proj):
-                P.apply(x[:T], rp[q], segs[d], ys[q][:T], ws)
-        else:
-            P.apply_multi(x[:T], rp, segs[d], [yq[:T] for yq in ys], ws)
-
-    def step(k, ev=None):
-        d = k % len(draws)
-        if ev is not None:
-            ev[0].record()
-        if n_proj == 1:
-            # segmentation and apply in one call (one launch for decode-sized
-            # batches; plora_segment then plora_apply otherwise)
-            T = draws[d].size
-            P.segment_apply(idx_dev[d], x[:T], reps[k % R][0], segs[d], ys[0][:T], ws)
-        else:
-            P.segment(idx_dev[d], segs[d])
-            apply_call(k)
-        if ev is not None:
-            ev[1].record()
-
-    for k in range(args.warmup):
-        step(k)
-    torch.cuda.synchronize()
-
     K = args.steps
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        step(args.warmup + k, evs[k])
-    torch.cuda.synchronize()
-    wall_eager = time.perf_counter() - t0
-    wall = wall_eager
-    step_event_s = None
+    n_proj = args.projections
+    if args.also == "auto":
+        extra = list(EXTRA_DEFAULT) if name == "decode" and n_proj == 1 else []
+    elif args.also in ("", "none"):
+        extra = []
+    else:
+        extra = [e for e in args.also.split(",") if e and e != name]
 
-    # ---- the same K steps launched as one HIP graph ------------------------------
-    # At decode size a step's two kernels take less GPU time than Python needs
-    # to issue them, so the eager loop measures the host.  The K steps (same
-    # draws, same stack replicas) are captured once and the graph is replayed:
-    # once untimed, then once timed.
-    if not args.eager:
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            for k in range(K):
-                step(args.warmup + k)
-        graph.replay()
-        torch.cuda.synchronize()
-        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
-        s0.record()
-        graph.replay()
-        s1.record()
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - t0
-        step_event_s = s0.elapsed_time(s1) / 1e3
+    b = ApplyBench(torch, P, W, dev, name, args, n_proj)
+    print(f"bench: {name} ({b.R} stack replicas, {b.RA} activation replicas)",
+          file=sys.stderr, flush=True)
+    m = b.measure(K, args.warmup, eager=args.eager, isolated=True, warm=True,
+                  ceiling=not args.no_ceiling)
+    placement = placement_split(torch, P, b, args, K) \
+        if args.pool_from >= 0 and n_proj == 1 else None
+    cpu = None if args.no_cpu_baseline else cpu_baseline(W, b, args)
+    rec = summary(b, m, K)
+    w, N, R, Tmax = b.w, b.N, b.R, b.Tmax
+    wps = b.wps
+    achieved = m["bytes_total"] / m["priced_s"] / 1e9
+    adapter_gbps = m["bytes_adapter"] / m["apply_s"] / 1e9
+    del b
+    torch.cuda.empty_cache()
 
-    apply_ms = np.array([a.elapsed_time(b) for a, b in evs])
-    ks = [(args.warmup + k) % len(draws) for k in range(K)]
-    tokens = sum(draws[d].size for d in ks)
-
-    # ---- the apply's own duration: K launches back to back -------------------
-    # (segments already built; the same draws and stack replicas as the steps).
-    # Events around single launches add several microseconds of their own at
-    # this size, so the launch stream is bracketed once around all K.
-    for k in range(K):
-        P.segment(idx_dev[k % len(draws)], segs[k % len(draws)])
-    torch.cuda.synchronize()
-    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-    def timed(separate=False):
-        # K calls captured as one graph (unless --eager), replayed once untimed
-        # and once between two events on the stream the kernels run on: at
-        # this size a Python loop of launches would time the host
-        if args.eager:
-            b0.record()
-            for k in range(K):
-                apply_call(k, separate)
-            b1.record()
-        else:
-            ga = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(ga):
-                for k in range(K):
-                    apply_call(k, separate)
-            ga.replay()
-            torch.cuda.synchronize()
-            b0.record()
-            ga.replay()
-            b1.record()
-        torch.cuda.synchronize()
-        return b0.elapsed_time(b1) / 1e3
-
-    apply_s = timed()
-    # warm: the same K calls on one stack replica, whose adapters stay in the
-    # 256 MB Infinity Cache from call to call (reported, never priced)
-    warm_s = None
-    if n_proj == 1 and R > 1:
-        saved_R, saved_reps = R, reps
-        R, reps = 1, reps[:1]
-        warm_s = timed()
-        R, reps = saved_R, saved_reps
-    separate_s = None
-    if n_proj > 1:                           # the same work as one call per projection
-        separate_s = timed(separate=True)
-    bytes_total = sum(tot_bytes[k % len(draws)] for k in range(K))
-    bytes_adapter = sum(ad_bytes[k % len(draws)] for k in range(K))
-    # the kernel the roofline prices: where a step is a single launch
-    # (plora_segment_apply's one-launch form) that launch, timed over the
-    # step graph; otherwise the apply's own launches
-    one_launch = (n_proj == 1 and step_event_s is not None and
-                  all(P.plora_segment_apply_launches(d.size, bases[0].struct) == 1
-                      for d in draws))
-    priced_s = step_event_s if one_launch else apply_s
-    kernel = ("segment_apply_kernel (plora_segment_apply)" if one_launch else
-              "plora_apply" if n_proj == 1 else "plora_apply_multi")
-    achieved = bytes_total / priced_s / 1e9
-    traffic = (measured_traffic(("plora_segment_apply_" if one_launch else "plora_apply_") + name)
-               if n_proj == 1 else None)
-    adapter_gbps = bytes_adapter / apply_s / 1e9
-
-    # ---- placement split: adapters K.. from the pinned host pool ----------------
-    placement = None
-    if args.pool_from >= 0 and n_proj == 1:
-        from paper_2608_05483_amd import placement as PL
-        Kp = args.pool_from
-        A_pool = torch.from_numpy(w.A.view(np.int16)).pin_memory()
-        B_pool = torch.from_numpy(w.B.view(np.int16)).pin_memory()
-        in_pool = np.arange(N) >= Kp
-        a_off = torch.from_numpy(np.where(in_pool, -1 - w.a_off, w.a_off).astype(np.int64)).to(dev)
-        b_off = torch.from_numpy(np.where(in_pool, -1 - w.b_off, w.b_off).astype(np.int64)).to(dev)
-        pool_reps = [P.Adapters(rp[0].A, rp[0].B, a_off, b_off, rp[0].ranks, rp[0].scales,
-                                w.h_in, w.h_out, w.max_rank, A_pool=A_pool, B_pool=B_pool)
-                     for rp in reps]
-
-        def pool_call(k, separate=False):
-            d = k % len(draws)
-            T = draws[d].size
-            P.apply(x[:T], pool_reps[k % R], segs[d], ys[0][:T], ws)
-
-        saved = apply_call
-        apply_call = pool_call
-        pool_s = timed()
-        apply_call = saved
-        hw = PL.Hardware()
-        model_split, model_hbm, pool_bytes = [], [], []
-        for d in draws:
-            ok = (d >= 0) & (d < N)
-            Bc = np.bincount(d[ok], minlength=N)
-            st = np.where(in_pool, PL.E2, PL.E1).astype(object)
-            model_split.append(PL.lora_time(Bc, w.ranks, st, w.h_in, w.h_out, hw))
-            model_hbm.append(PL.lora_time(Bc, w.ranks, np.full(N, PL.E1, dtype=object),
-                                          w.h_in, w.h_out, hw))
-            pool_bytes.append(sum(PL.adapter_bytes(w.ranks[a], w.h_in, w.h_out)
-                                  for a in np.unique(d[ok]) if a >= Kp))
-        placement = {
-            "pool_from": Kp,
-            "apply_us_split": round(pool_s / K * 1e6, 3),
-            "apply_us_all_hbm": round(apply_s / K * 1e6, 3),
-            "pool_bytes_per_call": int(np.mean(pool_bytes)),
-            "model_us_split": round(float(np.mean(model_split)) * 1e6, 3),
-            "model_us_all_hbm": round(float(np.mean(model_hbm)) * 1e6, 3),
-            "model_hardware": {"C_gpu": hw.C_gpu, "W_gpu": hw.W_gpu, "W_link": hw.W_link,
-                               "L_link": hw.L_link},
-        }
-
-    # ---- same-footprint plain-read ceiling -------------------------------------
-    ceiling = None
-    if not args.no_ceiling and n_proj == 1:
-        import ctypes
-        from paper_2608_05483_amd import build as B
-        pl = ctypes.CDLL(B.PROBE_LIB)
-        pl.plora_probe_read.argtypes = [ctypes.c_void_p] * 6 + [ctypes.c_int32] * 3 + \
-            [ctypes.c_void_p] * 2
-        pl.plora_probe_sink_words.argtypes = [ctypes.c_int32]
-        uniq = [torch.from_numpy(np.unique(d[(d >= 0) & (d < N)]).astype(np.int32)).to(dev)
-                for d in draws]
-        sink = torch.empty(pl.plora_probe_sink_words(max(u.numel() for u in uniq)),
-                           dtype=torch.int32, device=dev)
-        stream = torch.cuda.current_stream().cuda_stream
-
-        def probe(k):
-            d = k % len(draws)
-            rp = reps[k % R][0]
-            rc = pl.plora_probe_read(rp.A.data_ptr(), rp.B.data_ptr(), rp.a_off.data_ptr(),
-                                     rp.b_off.data_ptr(), rp.ranks.data_ptr(),
-                                     uniq[d].data_ptr(), uniq[d].numel(), w.h_in, w.h_out,
-                                     sink.data_ptr(), stream)
-            assert rc == 0
-
-        for k in range(args.warmup):
-            probe(k)
-        torch.cuda.synchronize()
-        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        p0.record()
-        for k in range(K):                   # back to back, as the apply is timed
-            probe(k)
-        p1.record()
-        torch.cuda.synchronize()
-        read_s = p0.elapsed_time(p1) / 1e3
-        bytes_adapter = sum(ad_bytes[k % len(draws)] for k in range(K))
-        ceiling = {"kernel": "plain 128-bit read of the same adapter blocks",
-                   "GBps": round(bytes_adapter / read_s / 1e9, 1),
-                   "us_per_launch": round(read_s / K * 1e6, 3),
-                   "frac_of_peak": round(bytes_adapter / read_s / 1e9 / HBM_PEAK_GBPS, 4)}
-
-    # ---- CPU oracle baseline ----------------------------------------------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
-        import oracle
-        cores = len(os.sched_getaffinity(0))
-        n_done, toks, t_cpu = 0, 0, 0.0
-        # cycle through the draws until the time budget is spent
-        while t_cpu < args.cpu_seconds:
-            d = draws[n_done % len(draws)]
-            wd = w if d.size == w.T else W.with_idx(w, d)
-            t1 = time.perf_counter()
-            for wp in wps:
-                oracle.apply(wd.x, d, wp.A, wp.a_off, wp.B, wp.b_off, wp.ranks, wp.scales,
-                             np.zeros((d.size, wp.h_out), np.uint16), w.h_in, wp.h_out,
-                             n_threads=cores)
-            t_cpu += time.perf_counter() - t1
-            toks += d.size
-            n_done += 1
-        # the same oracle on one thread, over a tenth of the time
-        t1_cpu, toks1, k1 = 0.0, 0, 0
-        while t1_cpu < args.cpu_seconds / 10:
-            d = draws[k1 % len(draws)]
-            wd = w if d.size == w.T else W.with_idx(w, d)
-            t1 = time.perf_counter()
-            for wp in wps:
-                oracle.apply(wd.x, d, wp.A, wp.a_off, wp.B, wp.b_off, wp.ranks, wp.scales,
-                             np.zeros((d.size, wp.h_out), np.uint16), w.h_in, wp.h_out,
-                             n_threads=1)
-            t1_cpu += time.perf_counter() - t1
-            toks1 += d.size
-            k1 += 1
-        model = "unknown"
-        try:
-            for line in open("/proc/cpuinfo"):
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
-                    break
-        except OSError:
-            pass
-        cpu = {"value": round(toks / t_cpu, 1), "unit": "tokens/s", "cores": cores,
-               "kind": "oracle",
-               "value_1_thread": round(toks1 / t1_cpu, 1),
-               "cpu_model": model,
-               "sample": f"{n_done} batches of this workload, cycling its "
-                         f"{len(draws)} token draws ({toks} tokens, {t_cpu:.1f} s), "
-                         f"fp32 C oracle, OpenMP over tokens on {cores} threads; "
-                         f"one thread: {k1} batches ({toks1} tokens, {t1_cpu:.1f} s)"}
+    configs = {}
+    for e in extra:
+        print(f"bench: {e}", file=sys.stderr, flush=True)
+        be = ApplyBench(torch, P, W, dev, e, args, 1)
+        me = be.measure(K, args.warmup, eager=args.eager, ceiling=not args.no_ceiling)
+        configs[e] = summary(be, me, K)
+        del be
+        torch.cuda.empty_cache()
 
     out = {
         "metric": "tokens/s and effective adapter GB/s (% of HBM peak) for plora_apply",
-        "value": round(tokens / wall, 1),
+        "value": round(m["tokens"] / m["wall"], 1),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
-        "ms_per_step": round(wall / K * 1e3, 5),
+        "ms_per_step": round(m["wall"] / K * 1e3, 5),
         "launch": "eager" if args.eager else "hip graph of the K steps",
-        "ms_per_step_eager": round(wall_eager / K * 1e3, 5),
+        "ms_per_step_eager": round(m["wall_eager"] / K * 1e3, 5),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(name, c) + (
+        "config": {"workload": describe(name, W.CONFIGS[name]) + (
                        "" if n_proj == 1 else
                        f"; {n_proj} projections sharing x, h_out "
                        f"{[wp.h_out for wp in wps]}, one plora_apply_multi call"),
-                   "T": int(Tmax), "h_in": w.h_in,
+                   "T": int(Tmax),
+                   "h_in": w.h_in,
                    "h_out": w.h_out if n_proj == 1 else [wp.h_out for wp in wps],
                    "max_rank": w.max_rank, "n_adapters": N,
-                   "draws": len(draws), "stack_replicas": R},
+                   "draws": args.draws, "stack_replicas": R,
+                   "activation_replicas": rec["activation_replicas"]},
         "adapter_GBps": round(adapter_gbps, 1),
         "adapter_frac_of_peak": round(adapter_gbps / HBM_PEAK_GBPS, 4),
-        "apply_us": round(apply_s / K * 1e6, 3),
-        "apply_us_warm": None if warm_s is None else round(warm_s / K * 1e6, 3),
-        "step_us_events": (None if step_event_s is None
-                           else round(step_event_s / K * 1e6, 3)),
-        "step_us_isolated_events": {
-            "mean": round(float(apply_ms.mean()) * 1e3, 3),
-            "p10": round(float(np.percentile(apply_ms, 10)) * 1e3, 3),
-            "p90": round(float(np.percentile(apply_ms, 90)) * 1e3, 3)},
-        "bytes_per_launch": int(bytes_total / K),
-        "adapter_bytes_per_launch": int(bytes_adapter / K),
+        "apply_us": rec["apply_us"],
+        "apply_us_warm": None if "warm_s" not in m else round(m["warm_s"] / K * 1e6, 3),
+        "step_us_events": round(m["step_s"] / K * 1e6, 3),
+        "step_us_isolated_events": m["isolated_us"],
+        "bytes_per_launch": rec["bytes_per_launch"],
+        "adapter_bytes_per_launch": rec["adapter_bytes_per_launch"],
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "kernel": kernel, "us_per_launch": round(priced_s / K * 1e6, 3)},
-        "read_ceiling": ceiling,
-        "separate_calls_us": (None if separate_s is None
-                              else round(separate_s / K * 1e6, 3)),
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": m["traffic"],
+                     "kernel": m["kernel"], "us_per_launch": rec["us_per_launch"]},
+        "read_ceiling": (None if "read_s" not in m else {
+            "kernel": "plain 128-bit read of the same adapter blocks, K launches in one graph",
+            "GBps": round(m["bytes_adapter"] / m["read_s"] / 1e9, 1),
+            "us_per_launch": rec["read_ceiling_us"],
+            "frac_of_peak": rec["read_ceiling_frac"]}),
+        "separate_calls_us": (None if "separate_s" not in m
+                              else round(m["separate_s"] / K * 1e6, 3)),
         "placement": placement,
+        "configs": configs,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
