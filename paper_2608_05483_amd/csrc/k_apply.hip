@@ -1,4 +1,6 @@
 // k_apply.hip -- plora_apply as one launch with the slice exchange.
+// every adapter byte is read once per call here: non-temporal reads
+#define PLORA_ADAPTER_POLICY 2
 #include "plora_dev.h"
 
 namespace plora_impl {

@@ -1,4 +1,6 @@
 // k_segapply.hip -- plora_segment_apply as one launch.
+// every adapter byte is read once per call here: non-temporal reads
+#define PLORA_ADAPTER_POLICY 2
 #include "plora_dev.h"
 
 namespace plora_impl {

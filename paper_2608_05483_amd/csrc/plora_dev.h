@@ -107,9 +107,21 @@ __device__ __forceinline__ Rsrc block_rsrc(const uint16_t* p, int64_t n) {
                                            kRsrcWord3);
 }
 
+// Cache policy of adapter reads, set by each kernel's source file before it
+// includes this header.  The exchange-form kernels read every byte of an
+// adapter's blocks once per call, so they read them non-temporally (2): the
+// caches then keep what is reused, the kernel's code, the token metadata and
+// the exchange words.  The other forms re-read A_i from the caches, once per
+// column slice or once per tile of a long segment, and keep the default (0).
+#ifndef PLORA_ADAPTER_POLICY
+#define PLORA_ADAPTER_POLICY 0
+#endif
+constexpr int kAdapterPolicy = PLORA_ADAPTER_POLICY;
+
 // 16 bytes at element e of the block, zero where !ok.
 __device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
-  const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (int)(e * 2) : kPastEnd, 0, 0);
+  const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (int)(e * 2) : kPastEnd, 0,
+                                                          kAdapterPolicy);
   return make_uint4((uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w);
 }
 
@@ -1076,7 +1088,7 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
       const bool ok = row < rows && oc * 8 < t.r;
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void*)(asrc + (ok ? row * t.r + oc * 8 : 0)),
-          (__attribute__((address_space(3))) void*)(base + 64 * i * 16), 16, 0, 0);
+          (__attribute__((address_space(3))) void*)(base + 64 * i * 16), 16, 0, kAdapterPolicy);
     }
 #pragma unroll
     for (int i = 0; i < NXI; ++i) {
