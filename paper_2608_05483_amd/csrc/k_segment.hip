@@ -376,6 +376,229 @@ __global__ void zero_kernel(uint4* p, size_t n16) {
     p[i] = make_uint4(0, 0, 0, 0);
 }
 
+// ---------------------------------------------------------------------------
+// the multi-work-group segmentation (batches above 1024 tokens)
+// ---------------------------------------------------------------------------
+//
+// The same stable counting sort by adapter id as the kernels above, spread
+// over G = ceil(T / 1024) work groups of 1024 tokens each, in three launches:
+//   count    group g histograms its tokens' keys in LDS (key = id, N for a
+//            skipped token) into row g of a G x (N + 2) table in the
+//            workspace; column N + 1 holds the group's tokens with id -1;
+//   scan     one work group sums each key's counts over the groups, writes
+//            each key's first position in the grouped order (the tokens of
+//            smaller keys) into row G of the table, and writes seg_ptr,
+//            seg_id, tiles and meta from the key totals;
+//   scatter  group g starts key k at that position plus key k's tokens in
+//            groups before g, and places each token there plus the number of
+//            equal keys before it in the group (token order), which is the
+//            stable order; skipped tokens fill the tail with -1.
+// The table is only read by the scan, so its loads are all in flight at
+// once (rewriting it in place would order each load behind a store).
+// Within a wavefront, tokens of equal key are found with ballots over the key
+// bits (peer masks): one LDS update per distinct key per wavefront.
+constexpr int kGroupTokens = 1024;
+constexpr int kGroupWaves = kGroupTokens / 64;
+constexpr int kGroupKeys = 8192;         // N + 1 keys must fit one LDS table
+constexpr int kMaxGroups = (PLORA_MAX_TOKENS + kGroupTokens - 1) / kGroupTokens;
+
+// sum over groups g < n (n <= kMaxGroups) of table[g][k]: every load issued
+// before any is used (from a clamped row, masked), so the sum costs one
+// memory round trip rather than one per group
+__device__ __forceinline__ int sum_rows(const int32_t* table, int S, int k, int n) {
+  int v[kMaxGroups];
+#pragma unroll
+  for (int g = 0; g < kMaxGroups; ++g) v[g] = table[(int64_t)(g < n ? g : 0) * S + k];
+  int s = 0;
+#pragma unroll
+  for (int g = 0; g < kMaxGroups; ++g) s += g < n ? v[g] : 0;
+  return s;
+}
+
+// The wavefront's lanes whose key equals this lane's (among lanes with in
+// set), from ballots over kbits key bits.
+__device__ __forceinline__ uint64_t key_peers(int key, bool in, int kbits) {
+  uint64_t peers = __ballot(in);
+  for (int b = 0; b < kbits; ++b) {
+    const bool bit = (key >> b) & 1;
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
+  }
+  return peers;
+}
+
+__device__ __forceinline__ int group_key(const int32_t* idx, int t, int T, int N, bool& none) {
+  none = false;
+  if (t >= T) return N + 1;
+  const int id = idx[t];
+  if (id >= 0 && id < N) return id;
+  none = id == -1;
+  return N;
+}
+
+// Exclusive scan of four ints per thread at once over a block of NW
+// wavefronts (one pass of barriers for all four); *total gets the sums.
+template <int NW>
+__device__ int4 block_exscan4(int4 v, int4* total, int4* sh /* [NW + 1] */) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int4 x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int a = __shfl_up(x.x, o, 64), b = __shfl_up(x.y, o, 64);
+    const int c = __shfl_up(x.z, o, 64), d = __shfl_up(x.w, o, 64);
+    if (lane >= o) { x.x += a; x.y += b; x.z += c; x.w += d; }
+  }
+  if (lane == 63) sh[w] = x;
+  __syncthreads();
+  if (w == 0) {
+    const int4 s = lane < NW ? sh[lane] : make_int4(0, 0, 0, 0);
+    int4 incl = s;
+#pragma unroll
+    for (int o = 1; o < NW; o <<= 1) {
+      const int a = __shfl_up(incl.x, o, 64), b = __shfl_up(incl.y, o, 64);
+      const int c = __shfl_up(incl.z, o, 64), d = __shfl_up(incl.w, o, 64);
+      if (lane >= o) { incl.x += a; incl.y += b; incl.z += c; incl.w += d; }
+    }
+    if (lane < NW) sh[lane] = make_int4(incl.x - s.x, incl.y - s.y, incl.z - s.z, incl.w - s.w);
+    if (lane == NW - 1) sh[NW] = incl;
+  }
+  __syncthreads();
+  const int4 b = sh[w];
+  *total = sh[NW];
+  return make_int4(x.x - v.x + b.x, x.y - v.y + b.y, x.z - v.z + b.z, x.w - v.w + b.w);
+}
+
+__global__ __launch_bounds__(kGroupTokens) void seg_count_kernel(
+    const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t kbits,
+    int32_t* __restrict__ table) {
+  __shared__ int32_t hist[kGroupKeys];
+  const int g = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int nb = N + 1;
+  for (int k = tid; k < nb; k += kGroupTokens) hist[k] = 0;
+  const int t = g * kGroupTokens + tid;
+  bool none;
+  const int key = group_key(idx, t, T, N, none);
+  const bool in = t < T;
+  const int n_none = __syncthreads_count(none);    // also orders the zeroing
+  const uint64_t peers = key_peers(key, in, kbits);
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  if (in && (peers & below) == 0) atomicAdd(&hist[key], __popcll(peers));
+  __syncthreads();
+  int32_t* row = table + (int64_t)g * (N + 2);
+  for (int k = tid; k < nb; k += kGroupTokens) row[k] = hist[k];
+  if (tid == 0) row[N + 1] = n_none;
+}
+
+__global__ __launch_bounds__(kGroupTokens) void seg_scan_kernel(
+    int32_t* __restrict__ table, int32_t G, int32_t T, int32_t N, int32_t cap,
+    int32_t tile_cap, int32_t* __restrict__ seg_ptr, int32_t* __restrict__ seg_id,
+    int32_t* __restrict__ meta, int4* __restrict__ tiles) {
+  constexpr int kPer = kGroupKeys / kGroupTokens;   // keys per thread, at most
+  __shared__ int4 scan_sh[kGroupWaves + 1];
+  __shared__ int32_t none_sh;
+  const int tid = threadIdx.x;
+  const int nb = N + 1, S = N + 2;
+  const int per = (nb + kGroupTokens - 1) / kGroupTokens;
+  const int k0 = tid * per;
+  int tot[kPer];
+  int mine = 0, mine_valid = 0, flags = 0, ntile = 0;
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int k = k0 + i;
+    int v = 0;
+    if (i < per && k < nb) v = sum_rows(table, S, k, G);
+    tot[i] = v;
+    mine += v;
+    if (k < N) {
+      mine_valid += v;
+      flags += v > 0;
+      ntile += (v + kTT - 1) / kTT;
+    }
+  }
+  if (tid == 0) none_sh = sum_rows(table, S, N + 1, G);
+  int4 tot4;
+  const int4 ex = block_exscan4<kGroupWaves>(make_int4(mine, mine_valid, flags, ntile), &tot4,
+                                             scan_sh);
+  int base = ex.x, sidx = ex.z, tu = ex.w;
+  const int n_valid = tot4.y, n_seg = tot4.z, n_tiles_all = tot4.w;
+  int32_t* starts = table + (int64_t)G * S;          // row G: each key's first position
+  const int n_none = none_sh;
+  const int n_invalid = T - n_valid - n_none;
+  const int n_tiles = min(n_tiles_all, tile_cap);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int k = k0 + i;
+    if (i < per && k < nb) {
+      starts[k] = base;
+      const int v = tot[i];
+      if (k < N && v > 0) {
+        seg_ptr[sidx] = base;
+        seg_id[sidx] = k;
+        for (int j = 0; j * kTT < v; ++j, ++tu)
+          if (tu < tile_cap) tiles[tu] = make_int4(k, base + j * kTT, min(kTT, v - j * kTT), sidx);
+        ++sidx;
+      }
+      base += v;
+    }
+  }
+  for (int q = n_seg + tid; q <= cap; q += kGroupTokens) seg_ptr[q] = n_valid;
+  for (int q = n_seg + tid; q < cap; q += kGroupTokens) seg_id[q] = -1;
+  for (int u = n_tiles + tid; u < tile_cap; u += kGroupTokens) tiles[u] = make_int4(-1, 0, 0, -1);
+  if (tid == 0) {
+    meta[0] = n_seg;
+    meta[1] = n_valid;
+    meta[2] = n_none;
+    meta[3] = n_invalid;
+    meta[4] = n_tiles;
+    meta[5] = 0;
+    meta[6] = 0;
+    meta[7] = 0;
+  }
+}
+
+__global__ __launch_bounds__(kGroupTokens) void seg_scatter_kernel(
+    const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t kbits,
+    const int32_t* __restrict__ table, int32_t* __restrict__ perm) {
+  __shared__ int32_t cursor[kGroupKeys];
+  const int g = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nb = N + 1, S = N + 2;
+  const int32_t* starts = table + (int64_t)gridDim.x * S;
+  for (int k = tid; k < nb; k += kGroupTokens) cursor[k] = starts[k] + sum_rows(table, S, k, g);
+  const int t = g * kGroupTokens + tid;
+  bool none;
+  const int key = group_key(idx, t, T, N, none);
+  const bool in = t < T;
+  const uint64_t peers = key_peers(key, in, kbits);
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  __syncthreads();
+  // wavefronts in token order, each taking its positions from the running
+  // cursors and advancing them (one lane per distinct key)
+  for (int ww = 0; ww < kGroupWaves; ++ww) {
+    if (w == ww && in) {
+      const int base = cursor[key];
+      perm[base + __popcll(peers & below)] = key < N ? t : -1;
+      __builtin_amdgcn_wave_barrier();
+      if ((peers & below) == 0) cursor[key] = base + __popcll(peers);
+    }
+    __syncthreads();
+  }
+}
+
+void launch_segment_groups(const int32_t* idx, int32_t T, int32_t N, int32_t cap,
+                           int32_t tile_cap, int32_t* perm, int32_t* seg_ptr, int32_t* seg_id,
+                           int32_t* meta, int4* tiles, int32_t* table, hipStream_t stream) {
+  const int G = (T + kGroupTokens - 1) / kGroupTokens;
+  int kbits = 0;
+  while ((1 << kbits) < N + 2) ++kbits;
+  hipLaunchKernelGGL(seg_count_kernel, dim3(G), dim3(kGroupTokens), 0, stream, idx, T, N, kbits,
+                     table);
+  hipLaunchKernelGGL(seg_scan_kernel, dim3(1), dim3(kGroupTokens), 0, stream, table, G, T, N,
+                     cap, tile_cap, seg_ptr, seg_id, meta, tiles);
+  // (seg_scatter_kernel's grid is G: it finds row G, the key starts, by it)
+  hipLaunchKernelGGL(seg_scatter_kernel, dim3(G), dim3(kGroupTokens), 0, stream, idx, T, N,
+                     kbits, table, perm);
+}
+
 void launch_segment(const int32_t* idx, int32_t T, int32_t N, int32_t cap, int32_t tile_cap,
                     int32_t tbits, int32_t key_bits, int32_t* perm, int32_t* seg_ptr,
                     int32_t* seg_id, int32_t* meta, int4* tiles, hipStream_t stream) {

@@ -120,6 +120,16 @@ struct WsLayout {
   size_t xep, counters, xw, vpart, total;
 };
 
+// Workspace bytes of the multi-work-group segmentation (batches above 1024
+// tokens over fewer than 8192 adapters: a table of (ceil(T / 1024) + 1) x
+// (N + 2) int32, the groups' counts and the keys' first positions); 0 where
+// plora_segment takes its one-work-group kernel.
+size_t segment_scratch_bytes(int32_t T, int32_t N) {
+  if (T <= 1024 || N < 0 || N + 1 > 8192) return 0;
+  const size_t groups = ((size_t)T + 1023) / 1024;
+  return (((groups + 1) * (size_t)(N + 2) * sizeof(int32_t)) + 255) & ~(size_t)255;
+}
+
 constexpr int kCounters = 2;   // workspace counters after the epochs (see ApplyArgs)
 
 constexpr size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -134,6 +144,9 @@ WsLayout ws_layout(int32_t T, const plora_adapters* ad, int n = 1) {
     if (ad[p].h_in <= 0 || ad[p].max_rank <= 0) return l;
     nvp = std::max(nvp, (size_t)ks_max_for(ad[p].h_in) * T * ad[p].max_rank * sizeof(float));
   }
+  // the last section also serves plora_segment_apply's segmentation, which
+  // runs before the partial sums are written
+  nvp = std::max(nvp, segment_scratch_bytes(T, ad->n_adapters));
   const int32_t tcap = plora_tile_capacity(T, ad->n_adapters);
   const size_t slots = (size_t)std::min(kXSlots, std::max(8, n * ((tcap + 7) & ~7)));
   l.xep = 0;
@@ -356,9 +369,12 @@ plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream)
   return launch_status();
 }
 
+size_t plora_segment_workspace_bytes(int32_t T, int32_t n_adapters) {
+  return segment_scratch_bytes(T, n_adapters);
+}
+
 plora_status plora_segment(const int32_t* idx, const plora_segments* seg, int32_t n_adapters,
                            void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws; (void)ws_bytes;
   if (!seg || n_adapters < 0) return PLORA_ERR_INVALID_ARG;
   plora_status st = check_segments_host(seg, n_adapters);
   if (st != PLORA_OK) return st;
@@ -370,8 +386,14 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg, int32_
   if (tbits + key_bits > 32) return PLORA_ERR_UNSUPPORTED;
   clear_stale_error();
   int4* tiles = reinterpret_cast<int4*>(seg->tiles);
-  launch_segment(idx, T, n_adapters, seg->cap, seg->tile_cap, tbits, key_bits, seg->perm,
-                 seg->seg_ptr, seg->seg_id, seg->meta, tiles, stream);
+  const size_t scratch = segment_scratch_bytes(T, n_adapters);
+  if (scratch > 0 && ws && aligned16(ws) && ws_bytes >= scratch) {
+    launch_segment_groups(idx, T, n_adapters, seg->cap, seg->tile_cap, seg->perm, seg->seg_ptr,
+                          seg->seg_id, seg->meta, tiles, reinterpret_cast<int32_t*>(ws), stream);
+  } else {
+    launch_segment(idx, T, n_adapters, seg->cap, seg->tile_cap, tbits, key_bits, seg->perm,
+                   seg->seg_ptr, seg->seg_id, seg->meta, tiles, stream);
+  }
   return launch_status();
 }
 
@@ -469,7 +491,11 @@ plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t 
   if (ldx < ad->h_in || ldy < ad->h_out) return PLORA_ERR_INVALID_ARG;
   if ((ldx & 7) || (ldy & 7) || !aligned16(x) || !aligned16(y)) return PLORA_ERR_UNSUPPORTED;
   if (!segment_apply_one_launch(T, ad)) {
-    st = plora_segment(idx, seg, ad->n_adapters, ws, ws_bytes, stream);
+    // the segmentation's scratch is the partial-sum section, free until the
+    // apply that follows on the same stream
+    const WsLayout l = ws_layout(T, ad);
+    st = plora_segment(idx, seg, ad->n_adapters, reinterpret_cast<char*>(ws) + l.vpart,
+                       ws_bytes - l.vpart, stream);
     if (st != PLORA_OK) return st;
     return plora_apply(x, ldx, ad, seg, y, ldy, ws, ws_bytes, stream);
   }

@@ -34,7 +34,7 @@ EXPORTED = ("plora_tile_capacity", "plora_workspace_bytes", "plora_workspace_ini
             "plora_check_adapters", "plora_status_string",
             "plora_debug_last_hip_error", "plora_debug_set_exchange_polls",
             "plora_pool_device_pointer", "plora_workspace_counters",
-            "plora_segment_apply_noalloc",
+            "plora_segment_apply_noalloc", "plora_segment_workspace_bytes",
             # include/plora_attention.h
             "plora_attn_partitions", "plora_attn_workspace_bytes", "plora_attn_partial",
             "plora_attn_merge", "plora_attn_decode")
@@ -87,6 +87,8 @@ def _load() -> ctypes.CDLL:
     L.plora_workspace_bytes.restype = sz
     L.plora_workspace_init.argtypes = [P, sz, P]
     L.plora_segment.argtypes = [P, SG, i32, P, sz, P]
+    L.plora_segment_workspace_bytes.argtypes = [i32, i32]
+    L.plora_segment_workspace_bytes.restype = sz
     L.plora_shrink.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_expand.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
     L.plora_apply.argtypes = [P, i64, AD, SG, P, i64, P, sz, P]
@@ -152,6 +154,10 @@ def plora_workspace_bytes(T: int, ad: plora_adapters) -> int:
 
 def plora_workspace_init(ws: int, ws_bytes: int, stream: int) -> None:
     _ok("plora_workspace_init", lib.plora_workspace_init(ws, ws_bytes, stream))
+
+
+def plora_segment_workspace_bytes(T: int, n_adapters: int) -> int:
+    return int(lib.plora_segment_workspace_bytes(T, n_adapters))
 
 
 def plora_segment(idx: int, seg: plora_segments, n_adapters: int, ws: int | None,
@@ -348,9 +354,16 @@ class Workspace:
         return plora_workspace_counters(self.ptr, self.nbytes, _stream(stream))
 
 
-def segment(idx, segs: Segments, stream=None) -> None:
-    plora_segment(idx.data_ptr(), segs.struct, segs.n_adapters, None, 0,
-                  _stream(stream))
+def segment(idx, segs: Segments, stream=None, ws=None) -> None:
+    """ws: an optional uint8 tensor (or Workspace) of at least
+    plora_segment_workspace_bytes bytes, for the many-work-group form."""
+    if isinstance(ws, Workspace):
+        ptr, n = ws.ptr, ws.nbytes
+    elif ws is not None:
+        ptr, n = ws.data_ptr(), ws.numel() * ws.element_size()
+    else:
+        ptr, n = None, 0
+    plora_segment(idx.data_ptr(), segs.struct, segs.n_adapters, ptr, n, _stream(stream))
 
 
 def shrink(x, ad: Adapters, segs: Segments, v, ws: Workspace, stream=None) -> None:

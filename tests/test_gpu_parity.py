@@ -211,18 +211,39 @@ def _seg_inputs():
     return cases
 
 
-@pytest.mark.parametrize("case", range(len(_seg_inputs())),
-                         ids=[c[0] for c in _seg_inputs()])
-def test_segment_bitwise(P, case):
+def _seg_forms():
+    """(case, form): every input in the one-work-group form, and in the
+    many-work-group form those it applies to (above 1024 tokens, fewer than
+    8192 ids)."""
+    out = []
+    for i, (name, idx, N) in enumerate(_seg_inputs()):
+        out.append((i, "one_group"))
+        if idx.size > 1024 and N + 1 <= 8192:
+            out.append((i, "groups"))
+    return out
+
+
+@pytest.mark.parametrize("case,form", _seg_forms(),
+                         ids=[f"{_seg_inputs()[i][0]}-{f}" for i, f in _seg_forms()])
+def test_segment_bitwise(P, case, form):
+    """Every output word equals the oracle's, in both forms: one work group
+    (no workspace) and, above 1024 tokens over fewer than 8192 adapters, the
+    three-launch many-work-group form (a workspace, here filled with garbage
+    first, since it needs no initial contents)."""
     name, idx, N = _seg_inputs()[case]
-    say(f"segment {name} T={idx.size} N={N}")
+    say(f"segment {name} T={idx.size} N={N} {form}")
 
     class R:
         pass
     run = R()
     run.idx, run.T = idx, idx.size
     run.segs = P.Segments(idx.size, N)
-    P.segment(dev(idx), run.segs)
+    ws = None
+    if form == "groups":
+        nbytes = P.plora_segment_workspace_bytes(idx.size, N)
+        assert nbytes > 0
+        ws = torch.full((nbytes,), 0x7f, dtype=torch.uint8, device="cuda")
+    P.segment(dev(idx), run.segs, ws=ws)
     torch.cuda.synchronize()
     check_segments(P, run, N)
 
@@ -652,6 +673,8 @@ def _segapply_cases():
         ("decode_desc", "decode", np.arange(64, dtype=np.int32)[::-1].copy() * 15),
         ("large", "large", None),
         ("tiny_two_calls", "tiny", None),
+        # above 1024 tokens: the many-work-group segmentation, then two launches
+        ("prefill_groups", "prefill", None),
     ]
 
 
