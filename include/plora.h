@@ -22,7 +22,7 @@
  *   plora_segment  group tokens by adapter id (stable counting sort)
  *   plora_shrink   v[t, :] = x[t, :] A_i            (E4's m = xA, fp32)
  *   plora_expand   y[t, :] += s_i v[t, :] B_i        (E4's y = mB)
- *   plora_apply    both: one launch for batches of up to 1024 tokens, two
+ *   plora_apply    both: one launch for batches of up to 256 tokens, two
  *                  above (per-slice partial sums of v, fp32, pass through the
  *                  workspace; within the one launch too when a tile is
  *                  split among several work groups)
@@ -243,8 +243,8 @@ plora_status plora_segment(const int32_t* idx, const plora_segments* seg,
  * (the rank-r reduction m = xA of strategy E4, section V-A).  Entries of v
  * for other tokens and columns are not written.  Two launches: the partial
  * sums over slices of h_in into ws (at least plora_workspace_bytes(T) bytes,
- * 16-byte aligned; one slice for T <= 1024), then their sum, in slice order,
- * into v.
+ * 16-byte aligned; one slice for T <= 256 outside the exchange form), then
+ * their sum, in slice order, into v.
  */
 plora_status plora_shrink(const uint16_t* x, int64_t ldx,
                           const plora_adapters* ad, const plora_segments* seg,
@@ -263,7 +263,7 @@ plora_status plora_expand(const float* v, int64_t ldv,
 /*
  * The apply: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for every valid token
  * (strategy E1: both matrices resident in GPU memory, section V-A).  For
- * T <= 1024 one launch; above, two launches with v's partial sums passed
+ * T <= 256 one launch; above, two launches with v's partial sums passed
  * through ws.  ws must hold plora_workspace_bytes(T) bytes, 16-byte aligned,
  * zeroed once by plora_workspace_init before its first use, in both cases.
  * When a batch has few tiles (the decode case), each tile is reduced by up

@@ -73,7 +73,9 @@ unsigned grid_for(const ApplyArgs& g, int s_max) {
   const int64_t cap8 = (g.tile_cap + 7) & ~7;
   if (g.fixed_slices > 0) return (unsigned)std::max<int64_t>(8, cap8 * g.fixed_slices);
   if (s_max <= 1) return (unsigned)std::max<int64_t>(8, cap8);
-  const int64_t spread = ((int64_t)g.slots * 4 / 3 + 8 + 7) & ~7;
+  // fit = round(kPlanItems slots / n8) >= 2 needs n8 <= 2/3 kPlanItems slots,
+  // so n8 fit <= 4/3 kPlanItems slots
+  const int64_t spread = ((int64_t)kPlanItems * g.slots * 4 / 3 + 8 + 7) & ~7;
   return (unsigned)std::max<int64_t>(8, std::min(cap8 * s_max, std::max(cap8, spread)));
 }
 

@@ -131,9 +131,9 @@ __device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
 //
 // Work items.  An item is one tile and one slice of h_in (KS slices of KR
 // rows) or of the y columns (JS slices of W columns), so that each launch
-// has about one item per resident work group (two per compute unit) and a
-// batch of a few dozen tiles still spreads over the whole chip.  plora_apply
-// takes one of three forms, by batch size:
+// has about kPlanItems items per resident work group and a batch of a few
+// dozen tiles still spreads over the whole chip.  plora_apply takes one of
+// three forms, by batch size:
 //
 //   one launch, S > 1 slices per tile (batches whose tile capacity is at
 //   most 2/3 of the resident work groups: decode batches).  S is chosen on
@@ -149,10 +149,12 @@ __device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
 //   its tile; the slices of a tile are numbered onto one XCD, so the first
 //   read brings A_i into that XCD's L2 and the others hit it.
 //
-//   two launches (larger batches, where x dominates): item (tile, h_in
+//   two launches (batches above kFusedTokens tokens): item (tile, h_in
 //   slice) writes its partial v to the workspace; item (tile, column slice)
 //   sums the tile's KS partials in slice order and expands.  Every byte of
-//   A_i, B_i and x is then read by one work group only.
+//   A_i, B_i and x is then read by one work group only, and a rank-64 tile's
+//   stream of A_i is split over KS items (the one-launch form above measured
+//   79.5 us on the ragged workload of 512 tokens, against 73 for this one).
 //
 // Grids are sized on the host for the most items any tile count up to the
 // capacity can produce; surplus work groups return after one load.
@@ -203,7 +205,13 @@ constexpr int kBufElems = kW * kWaveRing / 2 + 16;   // slack for transposed rea
 static_assert(kBufElems >= kChunk, "the LDS buffer also stages B_i chunks and the x window");
 constexpr int kRK = 32;              // MFMA K step
 constexpr int kMinSlice = 512;       // fewest y columns per work item (but h_out)
-constexpr int kFusedTokens = 1024;   // largest batch plora_apply runs as one launch
+constexpr int kFusedTokens = 256;    // largest batch plora_apply runs as one launch
+// Items per resident work group the device-chosen plans aim at: two, so that
+// the work groups that finish early (low-rank tiles) take more items while the
+// long ones (rank 64, long segments) run; one per work group measured 73 us on
+// the ragged workload, two 67, four 79 (the per-item latency chain then
+// outweighs the balance).
+constexpr int kPlanItems = 2;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -279,7 +287,7 @@ __device__ __forceinline__ Plan make_plan(const ApplyArgs& g, SliceKind kind) {
   if (g.fixed_slices > 0) {
     ks = js = g.fixed_slices;
   } else if (n8 > 0) {
-    const int fit = (g.slots + n8 / 2) / n8;
+    const int fit = (kPlanItems * g.slots + n8 / 2) / n8;
     ks = max(1, min(g.ks_max, fit));
     js = max(1, min(g.js_max, fit));
   }

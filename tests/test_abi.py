@@ -343,7 +343,7 @@ def test_segment_apply_launch_count():
     assert P.plora_segment_apply_launches(1, dec) == 1
     assert P.plora_segment_apply_launches(65, dec) == 1     # the whole work group segments
     assert P.plora_segment_apply_launches(256, dec) == 1
-    assert P.plora_segment_apply_launches(257, dec) == 2    # segment, then one apply launch
+    assert P.plora_segment_apply_launches(257, dec) == 3    # segment, then two apply launches
     assert P.plora_segment_apply_launches(4096, dec) == 3   # segment, then two apply launches
     assert P.plora_segment_apply_launches(8, _ad()) == 2    # h = 256: no split form
     assert P.plora_segment_apply_launches(0, dec) == 0
