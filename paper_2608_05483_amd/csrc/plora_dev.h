@@ -772,12 +772,24 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
         for (int jb = 0; jb < BP; jb += kCH) fma_b<TG>(d, bpre + jb, sm, m, jb);
         jb0 = BP;
       }
-      for (int jb = jb0; jb < m.njb; jb += kCH) {
-        uint4 b[kCH];
+      // the remaining rows in batches of kCH, the next batch always requested
+      // before the current one is used (rows past njb load nothing)
+      if (jb0 < m.njb) {
+        uint4 b0[kCH], b1[kCH];
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
-          b[j] = bld16(rb, be + (int64_t)(jb + j) * bstep, jb + j < m.njb);
-        fma_b<TG>(d, b, sm, m, jb);
+          b0[j] = bld16(rb, be + (int64_t)(jb0 + j) * bstep, jb0 + j < m.njb);
+        for (int jb = jb0; jb < m.njb; jb += 2 * kCH) {
+#pragma unroll
+          for (int j = 0; j < kCH; ++j)
+            b1[j] = bld16(rb, be + (int64_t)(jb + kCH + j) * bstep, jb + kCH + j < m.njb);
+          fma_b<TG>(d, b0, sm, m, jb);
+#pragma unroll
+          for (int j = 0; j < kCH; ++j)
+            b0[j] = bld16(rb, be + (int64_t)(jb + 2 * kCH + j) * bstep,
+                          jb + 2 * kCH + j < m.njb);
+          fma_b<TG>(d, b1, sm, m, jb + kCH);
+        }
       }
     }
     // all-reduce across the row slots of each column octet
@@ -1410,8 +1422,7 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     const int njt = S / 16;
     store_b(j0);
     lds_sync();
-    // y words of this chunk (the first came before), then the next chunk of B_i
-    if (ch > 0) expand_load_y<MT>(g, t, j0, JC, toks, pre);
+    // the next chunk of B_i (this chunk's y words came before)
     if (ch + 1 < nchunks) expand_load_b<MT>(g, t, j0 + JC, JC, pre);
     // every j tile's output words first, then every store: a use of a y
     // word after a store makes the compiler wait for that store too (the
@@ -1422,6 +1433,9 @@ __device__ __forceinline__ void expand_mfma(const ApplyArgs& g, const Tile& t, c
     if (nj > 4) expand_jtiles<8, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
     else if (nj > 2) expand_jtiles<4, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
     else expand_jtiles<2, MT>(Bs, S, vhi, vlo, RK, rk, w, njt, t.s, pre, out);
+    // this chunk's y words are used: request the next chunk's, which travel
+    // during the stores and the next chunk's staging
+    if (ch + 1 < nchunks) expand_load_y<MT>(g, t, j0 + JC, JC, toks, pre);
 #pragma unroll
     for (int i = 0; i < kJT; ++i) {
       const int jt = w + i * kW;
