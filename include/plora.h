@@ -103,8 +103,11 @@ typedef enum {
 #define PLORA_MAX_RANK 128
 /* Largest token batch one plora_segment call groups. */
 #define PLORA_MAX_TOKENS 16384
-/* Tokens per work tile; a segment longer than this is split into tiles. */
+/* Tokens per work tile: a segment longer than this is split into tiles.
+ * Batches of up to 256 tokens are tiled PLORA_SMALL_BATCH_TILE_TOKENS tokens
+ * at a time, larger ones PLORA_TILE_TOKENS at a time. */
 #define PLORA_TILE_TOKENS 32
+#define PLORA_SMALL_BATCH_TILE_TOKENS 2
 /* Most projections one plora_apply_multi call serves. */
 #define PLORA_MAX_PROJECTIONS 8
 /* Entries of plora_segments.meta. */
@@ -173,8 +176,9 @@ typedef struct {
  *              n_invalid (other ids outside [0, N)), n_tiles, 0, 0, 0}
  *   tiles      int32 [tile_cap][4]: the work tiles of the apply kernels,
  *              {adapter id, first perm position, length, segment index};
- *              a segment of L tokens gives ceil(L / PLORA_TILE_TOKENS) tiles;
- *              unused entries hold {-1, 0, 0, -1}
+ *              a segment of L tokens gives ceil(L / K) tiles, K =
+ *              PLORA_SMALL_BATCH_TILE_TOKENS for T <= 256, PLORA_TILE_TOKENS
+ *              above; unused entries hold {-1, 0, 0, -1}
  * One segmentation serves every projection and layer of a step that shares
  * the token batch.
  */
@@ -190,8 +194,9 @@ typedef struct {
   int32_t* tiles;
 } plora_segments;
 
-/* Host.  min(T, cap + T / PLORA_TILE_TOKENS) with cap = min(T, N): the most
- * tiles a batch of T tokens over N adapters can produce; 0 for T <= 0. */
+/* Host.  min(T, cap + T / K) with cap = min(T, N) and K the batch's tile
+ * length (see PLORA_TILE_TOKENS): the most tiles a batch of T tokens over N
+ * adapters can produce; 0 for T <= 0. */
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 
 /* Host.  Bytes of device workspace plora_apply and plora_shrink need for a

@@ -105,19 +105,20 @@ __global__ __launch_bounds__(NT) void segment_small_kernel(
   for (int q = n_seg + t; q <= cap; q += NT) seg_ptr[q] = n_valid;
   for (int q = n_seg + t; q < cap; q += NT) seg_id[q] = -1;
 
-  // tiles: a position starts one when it lies a multiple of kTT past its
-  // segment's start; sidx + sflag - 1 is the segment of position p
+  // tiles: a position starts one when it lies a multiple of the tile length
+  // past its segment's start; sidx + sflag - 1 is the segment of position p
   const int cur = sidx + (sflag ? 1 : 0) - 1;
   bool tflag = false;
   int start = 0, end = 0;
   if (p < n_valid) {
     start = start_s[cur];
     end = start_s[cur + 1];
-    tflag = ((p - start) % kTT) == 0;
+    tflag = ((p - start) % tile_tokens(T)) == 0;
   }
   int n_tiles;
   const int tu = block_exscan<NW>(tflag ? 1 : 0, &n_tiles, scan_sh);
-  if (tflag && tu < tile_cap) tiles[tu] = make_int4(key_p[p], p, min(kTT, end - p), cur);
+  if (tflag && tu < tile_cap)
+    tiles[tu] = make_int4(key_p[p], p, min(tile_tokens(T), end - p), cur);
   n_tiles = min(n_tiles, tile_cap);
   for (int u = n_tiles + t; u < tile_cap; u += NT) tiles[u] = make_int4(-1, 0, 0, -1);
   if (t == 0) {

@@ -353,7 +353,7 @@ extern "C" {
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters) {
   if (T <= 0) return 0;
   const int32_t cap = std::min(T, std::max(n_adapters, 0));
-  return std::min(T, cap + T / PLORA_TILE_TOKENS);
+  return std::min(T, cap + T / tile_tokens(T));
 }
 
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad) {

@@ -34,8 +34,18 @@
 
 namespace plora_impl {
 
-constexpr int kTT = PLORA_TILE_TOKENS;   // tokens per tile
+constexpr int kTT = PLORA_TILE_TOKENS;   // most tokens per tile
 static_assert((kTT & (kTT - 1)) == 0, "tile positions are taken modulo kTT with a mask");
+constexpr int kFusedTokens = 256;    // largest batch plora_apply runs as one launch
+// Tokens per tile by batch size.  Batches of up to kFusedTokens tokens (the
+// one-launch forms: decode) are cut into tiles of kSmallTile tokens, which the
+// vector path takes at every rank: with tiles of up to kTT tokens, a hot
+// adapter's tile of 3 to 14 tokens took the matrix path and finished about
+// 3 us after the single-token tiles, setting the launch's length.  A hot
+// adapter then has several tiles that read its blocks at the same time (the
+// repeats are cache hits).  Larger batches keep tiles of kTT tokens.
+constexpr int kSmallTile = PLORA_SMALL_BATCH_TILE_TOKENS;
+__host__ __device__ constexpr int tile_tokens(int T) { return T <= kFusedTokens ? kSmallTile : kTT; }
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
 // Groups of 64 words per wave in the radix passes: each wave owns a chunk of
@@ -205,7 +215,6 @@ constexpr int kBufElems = kW * kWaveRing / 2 + 16;   // slack for transposed rea
 static_assert(kBufElems >= kChunk, "the LDS buffer also stages B_i chunks and the x window");
 constexpr int kRK = 32;              // MFMA K step
 constexpr int kMinSlice = 512;       // fewest y columns per work item (but h_out)
-constexpr int kFusedTokens = 256;    // largest batch plora_apply runs as one launch
 // Items per resident work group the device-chosen plans aim at: two, so that
 // the work groups that finish early (low-rank tiles) take more items while the
 // long ones (rank 64, long segments) run; one per work group measured 73 us on
@@ -1881,7 +1890,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const int sstart = vp ? 63 - __clzll(smask & upto) : 0;
   const uint64_t later = smask & ~upto;
   const int send = later ? __ffsll((long long)later) - 1 : n_valid;   // segment end
-  const bool tflag = vp && ((lane - sstart) % kTT) == 0;
+  const bool tflag = vp && ((lane - sstart) % kSmallTile) == 0;
   const uint64_t tmask = __ballot(tflag);
   const int tu = __popcll(tmask & below);                 // tile starting here
   const int n_tiles = min(__popcll(tmask), so.tile_cap);
@@ -1893,7 +1902,8 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
     }
     for (int q = n_seg + lane; q <= so.cap; q += 64) so.seg_ptr[q] = n_valid;
     for (int q = n_seg + lane; q < so.cap; q += 64) so.seg_id[q] = -1;
-    if (tflag && tu < so.tile_cap) so.tiles[tu] = make_int4(kp, lane, min(kTT, send - lane), cur);
+    if (tflag && tu < so.tile_cap)
+      so.tiles[tu] = make_int4(kp, lane, min(kSmallTile, send - lane), cur);
     for (int q = n_tiles + lane; q < so.tile_cap; q += 64) so.tiles[q] = make_int4(-1, 0, 0, -1);
     if (lane < 8)
       so.meta[lane] = lane == 0 ? n_seg : lane == 1 ? n_valid : lane == 2 ? n_none
@@ -1905,7 +1915,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const int p0 = mine ? __ffsll((long long)mine) - 1 : 0;
   const uint64_t after0 = smask & (p0 == 63 ? 0 : ~((uint64_t(2) << p0) - 1));
   const int end0 = after0 ? __ffsll((long long)after0) - 1 : n_valid;
-  const int L = mine ? min(kTT, end0 - p0) : 0;
+  const int L = mine ? min(kSmallTile, end0 - p0) : 0;
   lt.rank_of[lane] = m_r;
   lt.scale_of[lane] = m_s;
   lt.ao_of[lane] = m_ao;
@@ -1985,7 +1995,7 @@ __device__ __forceinline__ void block_segment(const ApplyArgs& g, const int32_t*
   const uint64_t later = smask & ~upto;
   int send = later ? 64 * wv + __ffsll((long long)later) - 1 : first_after;
   send = min(send, n_valid);                                  // segment end
-  const bool tflag = vp && ((tid - sstart) % kTT) == 0;
+  const bool tflag = vp && ((tid - sstart) % kSmallTile) == 0;
   const uint64_t tmask_w = __ballot(tflag);
   if (lane == 0) lt.wcount[1][wv] = __popcll(tmask_w);
   lds_sync();
@@ -1997,7 +2007,7 @@ __device__ __forceinline__ void block_segment(const ApplyArgs& g, const int32_t*
   }
   const int tu = tiles_before + __popcll(tmask_w & below);  // tile starting here
   const int n_tiles = min(n_tiles_all, so.tile_cap);
-  const int tlen = min(kTT, send - tid);
+  const int tlen = min(kSmallTile, send - tid);
   if (write) {
     if (in) so.perm[tid] = vp ? tp : -1;
     if (sflag) {

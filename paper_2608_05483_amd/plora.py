@@ -24,6 +24,12 @@ PLORA_ERR_HIP = 4
 PLORA_MAX_RANK = 128
 PLORA_MAX_TOKENS = 16384
 PLORA_TILE_TOKENS = 32
+PLORA_SMALL_BATCH_TILE_TOKENS = 2
+
+
+def tile_tokens(T: int) -> int:
+    """Tokens per tile of a batch of T tokens (include/plora.h)."""
+    return PLORA_SMALL_BATCH_TILE_TOKENS if T <= 256 else PLORA_TILE_TOKENS
 PLORA_META_WORDS = 8
 PLORA_MAX_PROJECTIONS = 8
 

@@ -47,11 +47,13 @@ def test_tile_capacity():
     assert P.plora_tile_capacity(0, 10) == 0
     assert P.plora_tile_capacity(64, 1000) == 64
     assert P.plora_tile_capacity(8192, 32) == 32 + 8192 // 32
-    assert P.plora_tile_capacity(5, 1) == 1
-    # the bound holds for the worst batch: every segment of length 32k+1
-    for T, N in [(100, 3), (1000, 7), (16384, 1000)]:
+    assert P.plora_tile_capacity(5, 1) == 3            # tiles of 2 tokens up to 256
+    assert P.plora_tile_capacity(300, 1) == 1 + 300 // 32
+    # the bound holds for the worst batch: every segment of length Kk+1
+    for T, N in [(100, 3), (256, 7), (1000, 7), (16384, 1000)]:
         cap = min(T, N)
-        assert P.plora_tile_capacity(T, N) >= min(T, cap + T // 32)
+        K = P.tile_tokens(T)
+        assert P.plora_tile_capacity(T, N) >= min(T, cap + T // K)
 
 
 def _ad(**kw):

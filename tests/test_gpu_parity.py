@@ -174,12 +174,15 @@ def check_segments(P, run, N):
     n_tiles = int(meta[4])
     assert n_tiles <= s.tile_cap
     pos = 0
+    tl = P.tile_tokens(T)
     for k in range(n_tiles):
         a, p0, L, sg = tiles[k]
-        assert p0 == pos and 1 <= L <= P.PLORA_TILE_TOKENS
+        assert p0 == pos and 1 <= L <= tl
         assert o.seg_ptr[sg] <= p0 and p0 + L <= o.seg_ptr[sg + 1]
         assert a == o.seg_id[sg]
-        assert (p0 - o.seg_ptr[sg]) % P.PLORA_TILE_TOKENS == 0
+        assert (p0 - o.seg_ptr[sg]) % tl == 0
+        # tiles are as long as the segment allows
+        assert L == min(tl, o.seg_ptr[sg + 1] - p0)
         pos += L
     assert pos == int(o.meta[1])
     assert (tiles[n_tiles:] == np.array([-1, 0, 0, -1])).all()
