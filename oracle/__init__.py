@@ -24,6 +24,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "plora_oracle.c")
 _LIB = os.path.join(_HERE, "libplora_oracle.so")
+# AddressSanitizer build (clang, its ASan runtime preloaded by the caller;
+# single-threaded: the results do not depend on the thread count)
+ASAN_LIB = os.path.join(_HERE, "_build", "asan", "libplora_oracle.so")
+ASAN_CC = "/opt/rocm/llvm/bin/clang"
 
 # -O2 with no FMA contraction and no fast-math: each product and each sum is
 # rounded exactly once, in the order the source states.
@@ -42,13 +46,25 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_asan() -> str:
+    """Compile the oracle with AddressSanitizer into oracle/_build/asan."""
+    os.makedirs(os.path.dirname(ASAN_LIB), exist_ok=True)
+    tmp = ASAN_LIB + ".tmp%d" % os.getpid()
+    flags = [f for f in CFLAGS if f not in ("-fopenmp", "-O2")]
+    subprocess.check_call([ASAN_CC, "-O1", "-g", "-fsanitize=address",
+                           "-fno-omit-frame-pointer", *flags, _SRC, "-o", tmp, "-lm"])
+    os.replace(tmp, ASAN_LIB)
+    return ASAN_LIB
+
+
 _lib = None
 
 
 def lib() -> ctypes.CDLL:
     global _lib
     if _lib is None:
-        path = build(force=False)
+        # PLORA_ORACLE_LIB names another build to load (the sanitizer test's)
+        path = os.environ.get("PLORA_ORACLE_LIB") or build(force=False)
         L = ctypes.CDLL(path)
         P = ctypes.c_void_p
         i32, i64 = ctypes.c_int32, ctypes.c_int64

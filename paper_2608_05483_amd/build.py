@@ -77,5 +77,40 @@ def is_built() -> bool:
     return os.path.exists(LIB)
 
 
+# The same library with its host code instrumented by AddressSanitizer (the
+# device code is compiled as for the product), for the CPU sanitizer test;
+# loaded only with clang's ASan runtime preloaded (its __asan_* symbols are
+# left for that runtime to provide).
+ASAN_DIR = os.path.join(OBJ_DIR, "asan")
+ASAN_LIB = os.path.join(ASAN_DIR, "libplora.so")
+ASAN_HOST = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer"]
+
+
+def _asan_object(src: str, verbose: bool) -> str:
+    os.makedirs(ASAN_DIR, exist_ok=True)
+    obj = os.path.join(ASAN_DIR, os.path.basename(src) + ".o")
+    tmp = obj + ".tmp%d" % os.getpid()
+    _run([HIPCC, *CFLAGS, *ASAN_HOST, "-c", src, "-o", tmp], verbose)
+    os.replace(tmp, obj)
+    return obj
+
+
+def build_asan(verbose: bool = False) -> str:
+    """The host side (plora.hip: argument checks, workspace layout, plans)
+    compiled with the sanitizer, linked with the product build's objects of
+    the kernel files (whose host code is their launchers), built if absent."""
+    host = os.path.join(CSRC, "plora.hip")
+    others = [s for s in SRCS if s != host]
+    objs = [os.path.join(OBJ_DIR, os.path.basename(s) + ".o") for s in others]
+    missing = [s for s, o in zip(others, objs) if not os.path.exists(o)]
+    with ThreadPoolExecutor(max_workers=jobs()) as ex:
+        futs = [ex.submit(_asan_object, host, verbose)] + \
+               [ex.submit(_object, s, verbose) for s in missing]
+        asan_host = futs[0].result()
+        for f in futs[1:]:
+            f.result()
+    return _link([asan_host] + objs, ASAN_LIB, verbose)
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

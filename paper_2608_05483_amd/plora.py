@@ -74,17 +74,22 @@ class plora_segments(ctypes.Structure):
                 ("tiles", ctypes.c_void_p)]
 
 
+# PLORA_LIB names another build of the library to load instead (the
+# sanitizer test loads the AddressSanitizer build this way).
+LIB_PATH = os.environ.get("PLORA_LIB") or _build.LIB
+
+
 def _load() -> ctypes.CDLL:
-    if not os.path.exists(_build.LIB):
+    if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{_build.LIB} is not built; run `python -m paper_2608_05483_amd.build`")
+            f"{LIB_PATH} is not built; run `python -m paper_2608_05483_amd.build`")
     # torch ships its own libamdhip64 whose dependants name it without the
     # ".7" suffix; if this library (linked against the system runtime) were
     # loaded first, the process would end up with two HIP runtimes and torch's
     # streams and allocations would be foreign to our launches.  Loading torch
     # first makes the dynamic linker bind libplora.so to torch's runtime.
     import torch  # noqa: F401
-    L = ctypes.CDLL(_build.LIB)
+    L = ctypes.CDLL(LIB_PATH)
     P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     AD, SG = ctypes.POINTER(plora_adapters), ctypes.POINTER(plora_segments)
     L.plora_tile_capacity.argtypes = [i32, i32]
@@ -136,7 +141,6 @@ def _load() -> ctypes.CDLL:
 
 
 lib = _load()
-LIB_PATH = _build.LIB
 
 
 def _ok(fn: str, status: int) -> None:

@@ -32,7 +32,7 @@ def test_header_declares_the_expected_calls():
 
 
 def test_library_exports_every_declared_symbol():
-    lib = ctypes.CDLL(B.LIB)
+    lib = ctypes.CDLL(P.LIB_PATH)
     for fn in declared_functions():
         assert hasattr(lib, fn), fn
 
