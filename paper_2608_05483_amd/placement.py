@@ -12,7 +12,7 @@ of its four strategies exist here:
 decision, host logic only:
 
 * ``cost_e1`` / ``cost_e2`` / ``lora_time``: the E1 and E2 rows of the
-  per-strategy cost table (section VI-B), with the host link's bandwidth
+  per-strategy cost terms (Table IV, section VI-B), with the host link's bandwidth
   ``W_link`` and round trip ``L_link`` in place of the CXL link's, and the
   square model dimension D generalised to h_in and h_out (4 B D R flops
   become 2 B R (h_in + h_out), 2 D S R bytes become S R (h_in + h_out));

@@ -5,7 +5,7 @@ stacks, ranks, offsets and scales, as bf16 bit patterns (uint16) plus int and
 fp32 arrays.  It holds none of the apply's arithmetic, so the CPU oracle and
 the HIP path can both be fed from it without sharing any computation.
 
-The paper's evaluation (section VII-A, workload table) draws requests over
+The paper's evaluation (section VII-A, Table VII) draws requests over
 1000 adapters either uniformly or skewed (80% of requests to 50 adapters),
 with ranks drawn from {8, 16, 32, 64, 128} and model dimensions 4096 to 16384
 (section V-A).  Its traces (LMSYS Chatbot Arena) are not available; the five

@@ -1,5 +1,5 @@
 """The placement decision (strategies E1 / E2 of section V-A): the cost
-terms against the printed table at h_in = h_out = D and hand-worked values,
+terms against the rows Table IV prints, at h_in = h_out = D and hand-worked values,
 the temperature metric's closed form, and the selection's behaviour and
 invariants.  CPU only."""
 import numpy as np
