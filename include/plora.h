@@ -225,7 +225,8 @@ plora_status plora_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream)
 /* Host.  Bytes of workspace with which plora_segment groups a batch of T
  * tokens over N adapters with many work groups (three launches) instead of
  * one: (ceil(T / 1024) + 1) * (N + 2) int32, rounded up to 256 bytes, for
- * T > 1024 and N < 8192; 0 otherwise (one work group, no workspace).
+ * T > 1024 and 2048 <= N < 8192; 0 otherwise (one work group, one launch, no
+ * workspace: a counting sort for N < 2048, else a radix sort).
  * plora_workspace_bytes(T, ad) covers it for a stack of N adapters. */
 size_t plora_segment_workspace_bytes(int32_t T, int32_t n_adapters);
 
@@ -234,10 +235,10 @@ size_t plora_segment_workspace_bytes(int32_t T, int32_t n_adapters);
  * seg_id, meta and tiles (seg->T, cap and tile_cap must be set).  This is the
  * per-adapter batch of the cost model (section VI-B).  ws may be NULL; given
  * at least plora_segment_workspace_bytes(T, N) bytes (16-byte aligned, no
- * initial contents needed, overwritten), a batch above 1024 tokens is
- * grouped by many work groups in three launches, else by one work group in
- * one launch.  Both give the same output, bitwise deterministic; equal ids
- * keep their token order.
+ * initial contents needed, overwritten), a batch above 1024 tokens over
+ * 2048 to 8191 adapters is grouped by many work groups in three launches;
+ * every other batch by one work group in one launch.  Every form gives the
+ * same output, bitwise deterministic; equal ids keep their token order.
  */
 plora_status plora_segment(const int32_t* idx, const plora_segments* seg,
                            int32_t n_adapters, void* ws, size_t ws_bytes,

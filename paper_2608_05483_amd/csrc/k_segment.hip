@@ -19,7 +19,7 @@ __device__ int block_exscan(int v, int* total, int* sh /* [NW + 1] */) {
     if (lane >= o) x += y;
   }
   if (lane == 63) sh[w] = x;
-  __syncthreads();
+  lds_sync();
   if (w == 0) {
     int s = lane < kSegWaves ? sh[lane] : 0;
     int incl = s;
@@ -31,10 +31,10 @@ __device__ int block_exscan(int v, int* total, int* sh /* [NW + 1] */) {
     if (lane < kSegWaves) sh[lane] = incl - s;
     if (lane == kSegWaves - 1) sh[kSegWaves] = incl;
   }
-  __syncthreads();
+  lds_sync();
   int res = x - v + sh[w];
   *total = sh[kSegWaves];
-  __syncthreads();
+  lds_sync();
   return res;
 }
 
@@ -88,7 +88,7 @@ __global__ __launch_bounds__(NT) void segment_small_kernel(
     key_p[rank] = key;
     perm[rank] = key < N ? t : -1;
   }
-  __syncthreads();
+  lds_sync();
 
   // segments: position p starts one when its key differs from p - 1's
   const int p = t;
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(NT) void segment_small_kernel(
     start_s[sidx] = p;
   }
   if (t == 0) start_s[n_seg] = n_valid;
-  __syncthreads();
+  lds_sync();
   for (int q = n_seg + t; q <= cap; q += NT) seg_ptr[q] = n_valid;
   for (int q = n_seg + t; q < cap; q += NT) seg_id[q] = -1;
 
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   const uint32_t tmask = (1u << tbits) - 1u;
 
   if (tid == 0) { n_none_sh = 0; n_invalid_sh = 0; }
-  __syncthreads();
+  lds_sync();
 
   // load and pack; count skipped tokens.  Eight loads per thread are issued
   // before any is used (addresses past T re-read idx[0]), so the batch costs
@@ -185,7 +185,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   }
   if (my_none) atomicAdd(&n_none_sh, my_none);
   if (my_invalid) atomicAdd(&n_invalid_sh, my_invalid);
-  __syncthreads();
+  lds_sync();
 
   // LSD radix passes over the key bits; each wave owns a contiguous chunk
   const int chunk = ((T + kSegWaves - 1) / kSegWaves + 63) & ~63;
@@ -198,7 +198,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   for (int pass = 0; pass < passes; ++pass) {
     const int shift = tbits + pass * dbits;
     for (int d = lane; d < nbuck; d += 64) cursor[w][d] = 0;
-    __syncthreads();
+    lds_sync();
     // count digits per wave; each group's words and peer masks stay in
     // registers for the scatter below (a wave has at most kSegGroups groups)
     uint32_t gword[kSegGroups];
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
         if (act && (peers & below) == 0ull) cursor[w][dig] += __popcll(peers);
       }
     }
-    __syncthreads();
+    lds_sync();
     // exclusive scan in (digit, wave) order
     {
       const int entries = nbuck * kSegWaves;
@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
         base += vals[i];
       }
     }
-    __syncthreads();
+    lds_sync();
     // stable scatter: groups of 64 in order, rank by lower peers
 #pragma unroll
     for (int gi = 0; gi < kSegGroups; ++gi) {
@@ -261,7 +261,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
         __builtin_amdgcn_wave_barrier();
       }
     }
-    __syncthreads();
+    lds_sync();
     uint32_t* tmp = buf0; buf0 = buf1; buf1 = tmp;
   }
 
@@ -315,7 +315,7 @@ __global__ __launch_bounds__(kSegThreads) void segment_kernel(
   }
   n_seg = min(n_seg, cap);
   if (tid == 0) seg_lds_ptr[n_seg] = n_valid;
-  __syncthreads();
+  lds_sync();
   for (int s = n_seg + tid; s <= cap; s += kSegThreads) seg_ptr[s] = n_valid;
   for (int s = n_seg + tid; s < cap; s += kSegThreads) seg_id[s] = -1;
 
@@ -428,6 +428,32 @@ __device__ __forceinline__ uint64_t key_peers(int key, bool in, int kbits) {
   return peers;
 }
 
+// key_peers for chunks of few distinct keys (a request's tokens are
+// contiguous, so a prefill chunk holds one or two): up to kLeaderRounds times
+// the first lane not yet matched takes every lane with its key (a ballot per
+// distinct key); lanes left over after that take key_peers' kbits ballots.
+// The two agree: every lane of a key matched in a round leaves together, so
+// the lanes left over share no key with those that left.
+constexpr int kLeaderRounds = 4;
+__device__ __forceinline__ uint64_t key_peers_few(int key, bool in, int kbits) {
+  uint64_t left = __ballot(in);
+  uint64_t peers = 0;
+#pragma unroll
+  for (int it = 0; it < kLeaderRounds; ++it) {
+    if (left == 0) break;                                   // wave-uniform
+    const int lead = __builtin_ctzll(left);
+    const int lk = __builtin_amdgcn_readlane(key, lead);
+    const uint64_t m = __ballot(key == lk) & left;
+    if ((m >> (threadIdx.x & 63)) & 1) peers = m;
+    left &= ~m;
+  }
+  if (left != 0) {                                          // wave-uniform
+    const uint64_t rest = key_peers(key, in, kbits);
+    if ((left >> (threadIdx.x & 63)) & 1) peers = rest;
+  }
+  return peers;
+}
+
 __device__ __forceinline__ int group_key(const int32_t* idx, int t, int T, int N, bool& none) {
   none = false;
   if (t >= T) return N + 1;
@@ -437,33 +463,47 @@ __device__ __forceinline__ int group_key(const int32_t* idx, int t, int T, int N
   return N;
 }
 
+// The value of the lane CTRL names (a DPP row shift or row broadcast), 0
+// where it names none or ROWS masks the lane's row of 16 lanes off.
+template <int CTRL, int ROWS = 0xf>
+__device__ __forceinline__ int dpp_or_zero(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, false);
+}
+
+// Inclusive scan over the wavefront's 64 lanes, of four ints at once, with
+// DPP moves (no LDS): shifts right by 1, 2, 4 and 8 lanes within each row of
+// 16 scan the rows; lane 15's total is then broadcast into rows 1 and 3, and
+// lane 31's (rows 0 and 1) into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += dpp_or_zero<0x111>(x);          // row_shr:1
+  x += dpp_or_zero<0x112>(x);          // row_shr:2
+  x += dpp_or_zero<0x114>(x);          // row_shr:4
+  x += dpp_or_zero<0x118>(x);          // row_shr:8
+  x += dpp_or_zero<0x142, 0xa>(x);     // row_bcast:15
+  x += dpp_or_zero<0x143, 0xc>(x);     // row_bcast:31
+  return x;
+}
+__device__ __forceinline__ int4 wave_incl_scan4(int4 v) {
+  return make_int4(wave_incl_scan(v.x), wave_incl_scan(v.y), wave_incl_scan(v.z),
+                   wave_incl_scan(v.w));
+}
+
 // Exclusive scan of four ints per thread at once over a block of NW
 // wavefronts (one pass of barriers for all four); *total gets the sums.
 template <int NW>
 __device__ int4 block_exscan4(int4 v, int4* total, int4* sh /* [NW + 1] */) {
+  static_assert(NW <= 64, "one wavefront scans the wavefront totals");
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int4 x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int a = __shfl_up(x.x, o, 64), b = __shfl_up(x.y, o, 64);
-    const int c = __shfl_up(x.z, o, 64), d = __shfl_up(x.w, o, 64);
-    if (lane >= o) { x.x += a; x.y += b; x.z += c; x.w += d; }
-  }
+  const int4 x = wave_incl_scan4(v);
   if (lane == 63) sh[w] = x;
-  __syncthreads();
+  lds_sync();
   if (w == 0) {
     const int4 s = lane < NW ? sh[lane] : make_int4(0, 0, 0, 0);
-    int4 incl = s;
-#pragma unroll
-    for (int o = 1; o < NW; o <<= 1) {
-      const int a = __shfl_up(incl.x, o, 64), b = __shfl_up(incl.y, o, 64);
-      const int c = __shfl_up(incl.z, o, 64), d = __shfl_up(incl.w, o, 64);
-      if (lane >= o) { incl.x += a; incl.y += b; incl.z += c; incl.w += d; }
-    }
+    const int4 incl = wave_incl_scan4(s);
     if (lane < NW) sh[lane] = make_int4(incl.x - s.x, incl.y - s.y, incl.z - s.z, incl.w - s.w);
     if (lane == NW - 1) sh[NW] = incl;
   }
-  __syncthreads();
+  lds_sync();
   const int4 b = sh[w];
   *total = sh[NW];
   return make_int4(x.x - v.x + b.x, x.y - v.y + b.y, x.z - v.z + b.z, x.w - v.w + b.w);
@@ -484,7 +524,7 @@ __global__ __launch_bounds__(kGroupTokens) void seg_count_kernel(
   const uint64_t peers = key_peers(key, in, kbits);
   const uint64_t below = (uint64_t(1) << lane) - 1;
   if (in && (peers & below) == 0) atomicAdd(&hist[key], __popcll(peers));
-  __syncthreads();
+  lds_sync();
   int32_t* row = table + (int64_t)g * (N + 2);
   for (int k = tid; k < nb; k += kGroupTokens) row[k] = hist[k];
   if (tid == 0) row[N + 1] = n_none;
@@ -571,7 +611,7 @@ __global__ __launch_bounds__(kGroupTokens) void seg_scatter_kernel(
   const bool in = t < T;
   const uint64_t peers = key_peers(key, in, kbits);
   const uint64_t below = (uint64_t(1) << lane) - 1;
-  __syncthreads();
+  lds_sync();
   // wavefronts in token order, each taking its positions from the running
   // cursors and advancing them (one lane per distinct key)
   for (int ww = 0; ww < kGroupWaves; ++ww) {
@@ -581,8 +621,175 @@ __global__ __launch_bounds__(kGroupTokens) void seg_scatter_kernel(
       __builtin_amdgcn_wave_barrier();
       if ((peers & below) == 0) cursor[key] = base + __popcll(peers);
     }
-    __syncthreads();
+    lds_sync();
   }
+}
+
+// ---------------------------------------------------------------------------
+// one-launch counting sort (256 < T <= PLORA_MAX_TOKENS, N < kCountKeys)
+// ---------------------------------------------------------------------------
+//
+// One 1024-thread work group; wavefront w owns a contiguous range of
+// ceil(T / 16) tokens (rounded up to whole 64-token chunks) and its own row
+// of key counts in LDS.
+//   count    each wavefront counts its range's keys into its row (the lanes
+//            of a chunk with equal key are found with ballots over the key
+//            bits; one of them adds the group's size), and keeps each chunk's
+//            keys and peer masks in registers;
+//   scan     each key's count is summed over the rows and the totals are
+//            scanned into segment starts; row w's entry for key k becomes the
+//            position of wavefront w's first token of key k (the key's start
+//            plus its tokens in earlier wavefronts); seg_ptr, seg_id, tiles
+//            and meta are written from the totals;
+//   scatter  each wavefront walks its chunks in token order, placing each
+//            token at its row's cursor for its key plus the number of equal
+//            keys before it in the chunk, then advancing the cursor.
+// Every wavefront writes only its own row after the scan, so the scatter needs
+// no barrier between wavefronts.  Same output bits as every other form.
+constexpr int kCountChunks =
+    (PLORA_MAX_TOKENS + kGroupWaves * 64 - 1) / (kGroupWaves * 64);   // chunks per wavefront
+
+__global__ __launch_bounds__(kGroupTokens) void segment_count_kernel(
+    const int32_t* __restrict__ idx, int32_t T, int32_t N, int32_t cap, int32_t tile_cap,
+    int32_t kbits, int32_t* __restrict__ perm, int32_t* __restrict__ seg_ptr,
+    int32_t* __restrict__ seg_id, int32_t* __restrict__ meta, int4* __restrict__ tiles) {
+  __shared__ __align__(16) int32_t rows[kGroupWaves][kCountKeys];
+  __shared__ int4 scan_sh[kGroupWaves + 1];
+  __shared__ int32_t none_sh;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nb = N + 1;
+  const int tl = tile_tokens(T);
+  const int per_w = ((T + kGroupWaves - 1) / kGroupWaves + 63) & ~63;   // tokens per wavefront
+  const int nch = per_w >> 6;                                             // chunks per wavefront
+  const uint64_t below = (uint64_t(1) << lane) - 1;
+  // the ids of every chunk, requested before anything else (they arrive
+  // while the rows are cleared)
+  int ids[kCountChunks];
+#pragma unroll
+  for (int c = 0; c < kCountChunks; ++c) {
+    const int t = w * per_w + c * 64 + lane;
+    ids[c] = idx[c < nch && t < T ? t : 0];
+  }
+  for (int k = lane * 4; k < nb; k += 256) *reinterpret_cast<int4*>(&rows[w][k]) = int4{0, 0, 0, 0};
+  if (tid == 0) none_sh = 0;
+  lds_sync();
+
+  // count
+  int keys[kCountChunks];
+  uint64_t peers[kCountChunks];
+  int my_none = 0;
+#pragma unroll
+  for (int c = 0; c < kCountChunks; ++c) {
+    keys[c] = N + 1;
+    peers[c] = 0;
+    if (c < nch) {                                  // wave-uniform
+      const int t = w * per_w + c * 64 + lane;
+      const bool in = t < T;
+      const int id = ids[c];
+      const bool valid = in && id >= 0 && id < N;
+      const int key = !in ? N + 1 : valid ? id : N;
+      my_none += in && id == -1;
+      const uint64_t pm = key_peers_few(key, in, kbits);
+      keys[c] = key;
+      peers[c] = pm;
+      // one lane per distinct key adds, so no two lanes share an address;
+      // an atomic with no return waits for nothing
+      if (in && (pm & below) == 0) atomicAdd(&rows[w][key], __popcll(pm));
+    }
+  }
+  if (my_none) atomicAdd(&none_sh, my_none);
+  lds_sync();
+
+  // scan: keys k0 .. k0 + per - 1 per thread
+  const int per = (nb + kGroupTokens - 1) / kGroupTokens;   // at most 2
+  const int k0 = tid * per;
+  int tot[2] = {0, 0};
+  int mine = 0, mine_valid = 0, flags = 0, ntile = 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int k = k0 + i;
+    if (i < per && k < nb) {
+      int v = 0;
+#pragma unroll
+      for (int ww = 0; ww < kGroupWaves; ++ww) v += rows[ww][k];
+      tot[i] = v;
+      mine += v;
+      if (k < N) {
+        mine_valid += v;
+        flags += v > 0;
+        ntile += (v + tl - 1) / tl;
+      }
+    }
+  }
+  int4 tot4;
+  const int4 ex = block_exscan4<kGroupWaves>(make_int4(mine, mine_valid, flags, ntile), &tot4,
+                                             scan_sh);
+  int base = ex.x, sidx = ex.z, tu = ex.w;
+  const int n_valid = tot4.y, n_seg = tot4.z, n_tiles = min(tot4.w, tile_cap);
+  const int n_none = none_sh;
+  const int n_invalid = T - n_valid - n_none;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int k = k0 + i;
+    if (i < per && k < nb) {
+      int run = base;
+#pragma unroll
+      for (int ww = 0; ww < kGroupWaves; ++ww) {
+        const int c = rows[ww][k];
+        rows[ww][k] = run;
+        run += c;
+      }
+      const int v = tot[i];
+      if (k < N && v > 0) {
+        seg_ptr[sidx] = base;
+        seg_id[sidx] = k;
+        for (int j = 0; j * tl < v; ++j, ++tu)
+          if (tu < tile_cap) tiles[tu] = make_int4(k, base + j * tl, min(tl, v - j * tl), sidx);
+        ++sidx;
+      }
+      base += v;
+    }
+  }
+  for (int q = n_seg + tid; q <= cap; q += kGroupTokens) seg_ptr[q] = n_valid;
+  for (int q = n_seg + tid; q < cap; q += kGroupTokens) seg_id[q] = -1;
+  for (int u = n_tiles + tid; u < tile_cap; u += kGroupTokens) tiles[u] = make_int4(-1, 0, 0, -1);
+  if (tid == 0) {
+    meta[0] = n_seg;
+    meta[1] = n_valid;
+    meta[2] = n_none;
+    meta[3] = n_invalid;
+    meta[4] = n_tiles;
+    meta[5] = 0;
+    meta[6] = 0;
+    meta[7] = 0;
+  }
+  lds_sync();
+
+  // scatter: each wavefront through its own chunks with its own row of cursors
+#pragma unroll
+  for (int c = 0; c < kCountChunks; ++c) {
+    if (c < nch) {
+      const int t = w * per_w + c * 64 + lane;
+      const int key = keys[c];
+      const uint64_t pm = peers[c];
+      if (t < T) {
+        const int b = rows[w][key];
+        perm[b + __popcll(pm & below)] = key < N ? t : -1;
+      }
+      __builtin_amdgcn_wave_barrier();
+      if (t < T && (pm & below) == 0) rows[w][key] += __popcll(pm);
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+}
+
+void launch_segment_count(const int32_t* idx, int32_t T, int32_t N, int32_t cap,
+                          int32_t tile_cap, int32_t* perm, int32_t* seg_ptr, int32_t* seg_id,
+                          int32_t* meta, int4* tiles, hipStream_t stream) {
+  int kbits = 0;
+  while ((1 << kbits) < N + 2) ++kbits;
+  hipLaunchKernelGGL(segment_count_kernel, dim3(1), dim3(kGroupTokens), 0, stream, idx, T, N,
+                     cap, tile_cap, kbits, perm, seg_ptr, seg_id, meta, tiles);
 }
 
 void launch_segment_groups(const int32_t* idx, int32_t T, int32_t N, int32_t cap,
@@ -609,6 +816,8 @@ void launch_segment(const int32_t* idx, int32_t T, int32_t N, int32_t cap, int32
   else if (T <= 256)
     hipLaunchKernelGGL(segment_small_kernel<256>, dim3(1), dim3(256), 0, stream, idx, T, N, cap,
                        tile_cap, tbits, perm, seg_ptr, seg_id, meta, tiles);
+  else if (N + 1 <= kCountKeys)
+    launch_segment_count(idx, T, N, cap, tile_cap, perm, seg_ptr, seg_id, meta, tiles, stream);
   else if (T <= 1024)
     hipLaunchKernelGGL(segment_small_kernel<1024>, dim3(1), dim3(1024), 0, stream, idx, T, N,
                        cap, tile_cap, tbits, perm, seg_ptr, seg_id, meta, tiles);

@@ -123,11 +123,12 @@ struct WsLayout {
 };
 
 // Workspace bytes of the multi-work-group segmentation (batches above 1024
-// tokens over fewer than 8192 adapters: a table of (ceil(T / 1024) + 1) x
+// tokens over 2048 to 8191 adapters: a table of (ceil(T / 1024) + 1) x
 // (N + 2) int32, the groups' counts and the keys' first positions); 0 where
-// plora_segment takes its one-work-group kernel.
+// plora_segment takes a one-work-group kernel (fewer adapters: the counting
+// sort of kCountKeys keys; more: the radix sort).
 size_t segment_scratch_bytes(int32_t T, int32_t N) {
-  if (T <= 1024 || N < 0 || N + 1 > 8192) return 0;
+  if (T <= 1024 || N < 0 || N + 1 <= kCountKeys || N + 1 > 8192) return 0;
   const size_t groups = ((size_t)T + 1023) / 1024;
   return (((groups + 1) * (size_t)(N + 2) * sizeof(int32_t)) + 255) & ~(size_t)255;
 }

@@ -51,6 +51,10 @@ constexpr int kSegWaves = kSegThreads / 64;
 // Groups of 64 words per wave in the radix passes: each wave owns a chunk of
 // ceil(T / kSegWaves) words rounded up to 64, at most this many groups.
 constexpr int kSegGroups = ((PLORA_MAX_TOKENS + kSegWaves - 1) / kSegWaves + 63) / 64;
+// Keys (N + 1: the adapters and "skipped") of the one-launch counting sort,
+// which segments batches above kFusedTokens tokens without a workspace; more
+// adapters take the radix kernel, or the multi-work-group sort given one.
+constexpr int kCountKeys = 2048;
 constexpr int kCH = 8;                   // 16-byte chunks per lane per batch
 constexpr size_t kMaxLds = 160 * 1024;   // LDS per CU on gfx950
 
@@ -2086,6 +2090,9 @@ inline void allow_lds(const void* kernel, std::atomic<bool>& done) {
 void launch_segment(const int32_t* idx, int32_t T, int32_t N, int32_t cap, int32_t tile_cap,
                     int32_t tbits, int32_t key_bits, int32_t* perm, int32_t* seg_ptr,
                     int32_t* seg_id, int32_t* meta, int4* tiles, hipStream_t stream);
+void launch_segment_count(const int32_t* idx, int32_t T, int32_t N, int32_t cap,
+                          int32_t tile_cap, int32_t* perm, int32_t* seg_ptr, int32_t* seg_id,
+                          int32_t* meta, int4* tiles, hipStream_t stream);
 void launch_segment_groups(const int32_t* idx, int32_t T, int32_t N, int32_t cap,
                            int32_t tile_cap, int32_t* perm, int32_t* seg_ptr, int32_t* seg_id,
                            int32_t* meta, int4* tiles, int32_t* table, hipStream_t stream);

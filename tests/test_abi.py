@@ -289,16 +289,17 @@ def test_segment_apply_host_checks():
 
 def test_segment_workspace_bytes():
     """The many-work-group segmentation's table: (ceil(T / 1024) + 1) x
-    (N + 2) int32, 256-byte rounded, above 1024 tokens over fewer than 8192
-    ids."""
+    (N + 2) int32, 256-byte rounded, above 1024 tokens over 2048 to 8191 ids
+    (fewer ids take the one-launch counting sort, which needs none)."""
     f = P.plora_segment_workspace_bytes
-    assert f(1024, 1000) == 0 and f(0, 5) == 0
-    assert f(1025, 1000) == (3 * 1002 * 4 + 255) // 256 * 256
-    assert f(16384, 7) == (17 * 9 * 4 + 255) // 256 * 256
+    assert f(1024, 3000) == 0 and f(0, 5) == 0
+    assert f(1025, 1000) == 0 and f(16384, 2047) == 0 and f(16384, 7) == 0
+    assert f(1025, 2048) == (3 * 2050 * 4 + 255) // 256 * 256
+    assert f(16384, 3000) == (17 * 3002 * 4 + 255) // 256 * 256
     assert f(5000, 8191) > 0 and f(5000, 8192) == 0
     # the apply's workspace covers it
-    ad = _ad(n_adapters=1000, h_in=256, h_out=256, max_rank=8)
-    assert P.plora_workspace_bytes(16384, ad) >= f(16384, 1000)
+    ad = _ad(n_adapters=3000, h_in=256, h_out=256, max_rank=8)
+    assert P.plora_workspace_bytes(16384, ad) >= f(16384, 3000)
 
 
 def test_segment_apply_noalloc_host_checks():

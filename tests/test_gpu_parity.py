@@ -204,10 +204,12 @@ def _seg_inputs():
         cases.append((name, W.draw_idx(name, 1000 + W.CONFIG_NAMES.index(name)),
                       W.CONFIGS[name].N))
     # sizes at and around each segmentation kernel's limit (64, 256, 1024
-    # tokens), with skipped ids mixed in and segments longer than one tile
+    # tokens; 2048 keys of the counting sort, 8192 of the many-work-group
+    # sort), with skipped ids mixed in and segments longer than one tile
     for T, N in [(2, 1), (63, 3), (64, 3), (65, 1000), (256, 2), (257, 50), (1024, 1),
                  (1024, 1000), (16384, 1000), (16384, 7), (5000, 40000), (1023, 1024),
-                 (1025, 2)]:
+                 (1025, 2), (1025, 2047), (16384, 2047), (1000, 3000), (1025, 2048),
+                 (16384, 3000), (3000, 8191), (2000, 8192), (1089, 5)]:
         idx = rng.integers(-1, N, size=T).astype(np.int32)
         cases.append((f"rand_T{T}_N{N}", idx, N))
     cases.append(("zipf_max", W.zipf_ids(rng, 16384, 1000, 1.0), 1000))
@@ -216,12 +218,12 @@ def _seg_inputs():
 
 def _seg_forms():
     """(case, form): every input in the one-work-group form, and in the
-    many-work-group form those it applies to (above 1024 tokens, fewer than
-    8192 ids)."""
+    many-work-group form those it applies to (above 1024 tokens, 2048 to 8191
+    ids)."""
     out = []
     for i, (name, idx, N) in enumerate(_seg_inputs()):
         out.append((i, "one_group"))
-        if idx.size > 1024 and N + 1 <= 8192:
+        if idx.size > 1024 and 2048 <= N < 8192:
             out.append((i, "groups"))
     return out
 
@@ -230,9 +232,11 @@ def _seg_forms():
                          ids=[f"{_seg_inputs()[i][0]}-{f}" for i, f in _seg_forms()])
 def test_segment_bitwise(P, case, form):
     """Every output word equals the oracle's, in both forms: one work group
-    (no workspace) and, above 1024 tokens over fewer than 8192 adapters, the
-    three-launch many-work-group form (a workspace, here filled with garbage
-    first, since it needs no initial contents)."""
+    (no workspace: the comparison sort up to 256 tokens, above it the
+    counting sort below 2048 adapters, else the comparison or radix sort) and,
+    above 1024 tokens over 2048 to 8191 adapters, the three-launch
+    many-work-group form (a workspace, here filled with garbage first, since
+    it needs no initial contents)."""
     name, idx, N = _seg_inputs()[case]
     say(f"segment {name} T={idx.size} N={N} {form}")
 
@@ -676,8 +680,8 @@ def _segapply_cases():
         ("decode_desc", "decode", np.arange(64, dtype=np.int32)[::-1].copy() * 15),
         ("large", "large", None),
         ("tiny_two_calls", "tiny", None),
-        # above 1024 tokens: the many-work-group segmentation, then two launches
-        ("prefill_groups", "prefill", None),
+        # above 1024 tokens: the counting-sort segmentation, then two launches
+        ("prefill_counting", "prefill", None),
     ]
 
 
