@@ -385,6 +385,11 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
 // adapters (the longest segments, at the lowest ids) are spread over the
 // chip; giving each XCD a contiguous range of tiles instead measured 10 us
 // slower on the ragged workload.
+//
+// In the two-launch form, an order that sends a long segment's consecutive
+// tiles (with one slice) to one XCD, so that its slice of A_i is fetched from
+// HBM once and then hit in that XCD's L2, cut the prefill shrink's HBM reads
+// by 30% but not its time, and made the ragged workload 1.5 us slower.
 __device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, SliceKind kind,
                                           int i, Tile& t, int& my_tok, int& slice) {
   const int per = 8 * (kind == kRowSlices ? p.KS : p.JS);
@@ -1036,6 +1041,18 @@ __device__ __forceinline__ void wait_vm() {
   __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (0x7 << 4) | (0xf << 8));
 }
 
+// Wait until at most min(n, K) stages of PER loads each are outstanding
+// (n wave-uniform; the count must be a constant of the instruction).
+template <int PER, int K>
+__device__ __forceinline__ void wait_vm_stages(int n) {
+  if constexpr (K == 0) {
+    wait_vm<0>();
+  } else {
+    if (n >= K) wait_vm<K * PER>();
+    else wait_vm_stages<PER, K - 1>(n);
+  }
+}
+
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 // LDS address (byte offset in the work group's LDS) of a pointer into it.
@@ -1070,9 +1087,11 @@ __device__ __forceinline__ u32x4_t lds_b128(uint32_t a) {
 // operands straight from global memory into a ring of D stages of its own
 // LDS (global_load_lds_dwordx4, no registers), D stages ahead of its matrix
 // cores; no wavefront waits for another until the final reduction.  Every
-// stage issues the same loads (a stage past the wavefront's last re-reads its
-// last, loads past the block re-read the stage's start), so the loads in
-// flight behind a stage are a constant number and the wait for it is exact.
+// stage issues the same number of loads (loads past the block re-read the
+// stage's start), and no stage past the wavefront's last is issued: the wait
+// for stage j counts the loads of the min(D - 1, n - 1 - j) stages issued
+// after it (n the wavefront's stages), so it is exact, and the ring's tail
+// waits for no loads of its own that nothing uses.
 // Rows of the last K step past the block are zeroed in LDS before use.
 // Writes v to sm.vs (fp32) and its high/low bf16 split to sm.vhl.
 template <int MT, int R>
@@ -1109,7 +1128,7 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
 
   // this wavefront's stage j into ring slot sl
   auto issue = [&](int j, int sl) {
-    const int st = w + min(j, my_n - 1) * kW;
+    const int st = w + j * kW;
     const int kr0 = t.k0 + st * SR;
     const int rows = min(SR, t.k1 - kr0);             // valid rows of A_i in the stage
     const uint16_t* asrc = t.Ai + (int64_t)kr0 * t.r;
@@ -1139,7 +1158,7 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
     asm volatile("" ::: "memory");
   };
   auto consume = [&](int j, int sl) {
-    wait_vm<(D - 1) * (NAI + NXI)>();
+    wait_vm_stages<NAI + NXI, D - 1>(my_n - 1 - j);
     const int st = w + j * kW;
     const int rows = min(SR, t.k1 - t.k0 - st * SR);
     char* base = ring + sl * STG;
@@ -1183,18 +1202,18 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
         }
       }
     }
-    issue(j + D, sl);
+    if (j + D < my_n) issue(j + D, sl);
   };
   if (my_n > 0) {
 #pragma unroll
-    for (int sl = 0; sl < D; ++sl) issue(sl, sl);
+    for (int sl = 0; sl < D; ++sl)
+      if (sl < my_n) issue(sl, sl);
     for (int j0 = 0; j0 < my_n; j0 += D) {
 #pragma unroll
       for (int sl = 0; sl < D; ++sl)
         if (j0 + sl < my_n) consume(j0 + sl, sl);
     }
   }
-  wait_vm<0>();                                     // the ring's last re-reads
   lds_sync();
 
   // pairwise tree over the wavefronts: 4 -> 2 -> 1 slots, fixed order
@@ -2049,6 +2068,42 @@ __device__ __forceinline__ float sum_parts(const ApplyArgs& g, const Plan& p, co
   return v;
 }
 
+// The tile's v into sm.vs, each entry summed from the partials as sum_parts
+// sums it (slice order, the same bits), with the loads of kSumBatch entries
+// per thread (every slice of each) issued before any is added, so that a
+// tile costs one memory round trip per batch rather than one per entry
+// (p.KS <= kMaxSlices: the host gives a tile at most 8 slices of h_in).
+constexpr int kSumBatch = 4;
+__device__ __forceinline__ void sum_parts_tile(const ApplyArgs& g, const Plan& p, const Tile& t,
+                                               const Smem& sm) {
+  const int n = t.L * t.r;
+  const int64_t step = (int64_t)g.T * g.max_rank;
+  for (int o0 = 0; o0 < n; o0 += kSumBatch * kNT) {
+    float part[kSumBatch][kMaxSlices];
+#pragma unroll
+    for (int i = 0; i < kSumBatch; ++i) {
+      const int o = o0 + i * kNT + threadIdx.x;
+      const int l = o < n ? o / t.r : 0, c = o < n ? o - l * t.r : 0;
+      const float* src = g.vpart + (int64_t)(t.p0 + l) * g.max_rank + c;
+#pragma unroll
+      for (int ks = 0; ks < kMaxSlices; ++ks)
+        part[i][ks] = o < n && ks < p.KS ? src[ks * step] : 0.f;
+    }
+#pragma unroll
+    for (int i = 0; i < kSumBatch; ++i) {
+      const int o = o0 + i * kNT + threadIdx.x;
+      if (o < n) {
+        const int l = o / t.r, c = o - l * t.r;
+        float v = part[i][0];
+#pragma unroll
+        for (int ks = 1; ks < kMaxSlices; ++ks)
+          if (ks < p.KS) v += part[i][ks];
+        sm.vs[c * kTT + l] = v;
+      }
+    }
+  }
+}
+
 // Expand launch: item (tile, y column slice) takes the tile's v from the
 // workspace partials (plora_apply) or from g.v (plora_expand) and expands it.
 template <bool FROM_PARTS>
@@ -2063,11 +2118,14 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
     return;
   }
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
-  for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
-    const int l = o / t.r, c = o - l * t.r;
-    if (FROM_PARTS) {
-      sm.vs[c * kTT + l] = sum_parts(g, p, t, l, c);
-    } else {
+  // (issuing the expand's first B_i and y loads before these, so that the
+  // three travel together, measured 3 us slower on the prefill workload and
+  // 1.5 us on the ragged one)
+  if (FROM_PARTS) {
+    sum_parts_tile(g, p, t, sm);
+  } else {
+    for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
+      const int l = o / t.r, c = o - l * t.r;
       const int tk = sm.tok[l];
       sm.vs[c * kTT + l] = tk >= 0 ? g.v[(int64_t)tk * g.ldv + c] : 0.f;
     }
