@@ -204,9 +204,10 @@ int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
  * sections, each starting on a 256-byte boundary:
  *   1. the epochs of the one-launch apply's tile slots: 336 64-bit words,
  *      then two 64-bit counters (see plora_workspace_counters);
- *   2. its exchange regions: 8 * 32 * 128 64-bit words for each of
- *      P = min(336, max(8, cap8)) tile slots, cap8 being
- *      plora_tile_capacity(T, N) rounded up to a multiple of 8;
+ *   2. its exchange regions: 8 * PLORA_SMALL_BATCH_TILE_TOKENS * 128
+ *      64-bit words (16 KiB) for each of P = min(336, max(8, cap8)) tile
+ *      slots, cap8 being plora_tile_capacity(T, N) rounded up to a
+ *      multiple of 8;
  *   3. the partial sums of v over up to 8 slices of h_in, fp32,
  *      K * T * max_rank * 4 bytes with K = min(8, max(1, h_in / 512)).
  * Sections 1 and 2 keep their offsets whatever T, the ranks or the slice
@@ -309,7 +310,7 @@ plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t 
  * plora_segment_apply for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): the same call without a workspace argument.  Its workspace is
- * a static device array of the library, 65 MiB on every GPU it runs on, held
+ * a static device array of the library, 5 MiB on every GPU it runs on, held
  * until the process ends, zero when the library is loaded and then carrying
  * the exchange's epochs from call to call.  Batches of at most 256 tokens;
  * a larger T returns PLORA_ERR_UNSUPPORTED before anything is launched.
@@ -391,7 +392,10 @@ plora_status plora_pool_device_pointer(const void* host, const void** device);
  *   counts[1]  tokens that kept y_base because their adapter entry breaks
  *              the contract (a rank outside [0, max_rank], or a block
  *              misaligned or outside its array), counted once per call;
- *              plora_expand counts only when it is given a workspace.
+ *              plora_expand counts only when it is given a workspace.  A
+ *              one-launch call (T <= 256) also skips and counts the tokens
+ *              of a tile longer than PLORA_SMALL_BATCH_TILE_TOKENS, which
+ *              plora_segment never writes for such a batch.
  * PLORA_ERR_INVALID_ARG for null pointers, PLORA_ERR_WORKSPACE_TOO_SMALL for
  * a buffer that cannot be a workspace, PLORA_ERR_HIP for a failed copy.
  * Not for the hot path. */

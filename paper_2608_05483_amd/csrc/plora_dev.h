@@ -879,12 +879,15 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
 constexpr int kMaxSlices = 8;            // most slices per tile in the one-launch form
 constexpr int kXSlots = 336;             // tile slots with an exchange region
 constexpr int kSpinLimit = 20000;        // polls of a partner's word before computing v alone
-constexpr int64_t kSlotWords = (int64_t)kMaxSlices * kTT * PLORA_MAX_RANK;   // words per slot
+// Words per slot: every entry of a tile of the one-launch form (at most
+// kSmallTile tokens, the tile length plora_segment gives batches of up to
+// kFusedTokens tokens) at the largest rank, kMaxSlices words each.
+constexpr int64_t kSlotWords = (int64_t)kMaxSlices * kSmallTile * PLORA_MAX_RANK;
 
 struct Xchg {
   int s, S, kr;          // this item's slice, the tile's slice count, rows of h_in per slice
   uint32_t tag;          // this call's tag for the tile slot
-  uint64_t* words;       // the slot's region: [kTT * PLORA_MAX_RANK][kMaxSlices]
+  uint64_t* words;       // the slot's region: [kSmallTile * PLORA_MAX_RANK][kMaxSlices]
   int polls;             // polls before giving up on a partner
 };
 
@@ -921,8 +924,9 @@ __device__ __forceinline__ void exchange_item(int b, int S, int& q, int& s) {
 // sum them in).  Entry o = l r + c of the tile keeps its kMaxSlices words
 // side by side, so one address serves all of them.  A word carrying this
 // call's tag never changes again during the call, so a poll simply reloads
-// every word of the entry.  Returns false, for the whole work group, if some
-// partner's word did not arrive in time; sm.vs is then undefined.
+// the entry's S live words (the launch's S slices; the words past them are
+// never read).  Returns false, for the whole work group, if some partner's
+// word did not arrive in time; sm.vs is then undefined.
 __device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const Xchg& xc) {
   const int n = t.L * t.r;
   const uint64_t tagw = (uint64_t)xc.tag << 32;
@@ -938,7 +942,7 @@ __device__ __forceinline__ bool exchange_v(const Tile& t, const Smem& sm, const 
     for (int it = 0; !ready && it <= xc.polls; ++it) {
       if (it > 0) __builtin_amdgcn_s_sleep(2);
 #pragma unroll
-      for (int q = 0; q < kMaxSlices; ++q) w[q] = xpoll(e + q);
+      for (int q = 0; q < kMaxSlices; ++q) w[q] = q < xc.S ? xpoll(e + q) : 0;
       ready = true;
 #pragma unroll
       for (int q = 0; q < kMaxSlices; ++q)
@@ -1768,6 +1772,13 @@ __device__ __forceinline__ void apply_item(const ApplyArgs& g, int s, int slot, 
     int my_tok;
     t.bad = false;
     if (!src(t, my_tok)) {
+      count_skipped(g, t, s);
+      return;
+    }
+    if (t.L > kSmallTile) {
+      // longer than the exchange region holds: not a tile plora_segment
+      // gives a batch this small; skipped and counted like an unusable entry
+      t.bad = true;
       count_skipped(g, t, s);
       return;
     }

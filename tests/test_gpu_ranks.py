@@ -217,3 +217,35 @@ def test_unusable_entries_are_counted(P):
     assert give_ups == 0
     # apply, then shrink (which counts too): two calls
     assert skipped == 2 * int(rows.sum())
+
+
+def test_overlong_one_launch_tile_is_skipped_and_counted(P):
+    """A one-launch call (T <= 256) holds each tile's partial v in an
+    exchange region sized for PLORA_SMALL_BATCH_TILE_TOKENS tokens; a tile
+    longer than that (which plora_segment never writes for such a batch) is
+    skipped, its tokens keep y_base and are counted, and every other tile
+    gives the bits of the unmodified segmentation."""
+    w = W.make_workload("decode", scale="parity", ranks=16, n_adapters=64,
+                        idx=np.full(40, 7, np.int32))
+    run = Run(P, w).segment()
+    y_ref = run.apply()
+    tiles = run.segs.tiles.view(-1, 4).cpu().numpy().copy()
+    n = int(run.segs.meta[4].item())
+    tl = P.PLORA_SMALL_BATCH_TILE_TOKENS
+    assert n == 40 // tl and (tiles[:n, 2] == tl).all()
+    L = 2 * tl + 1                                  # longer than any one-launch tile
+    keep = tiles[:n][tiles[:n, 1] >= L + 1]         # the tiles after positions 0..L
+    new = [(7, 0, L, 0), (7, L, 1, 0)] + [tuple(t) for t in keep]
+    tiles[:] = (-1, 0, 0, -1)
+    tiles[:len(new)] = new
+    run.segs.tiles.copy_(torch.from_numpy(tiles.reshape(-1)))
+    run.segs.meta[4] = len(new)
+    run.ws = P.Workspace(w.T, run.ad)
+    y = run.apply()
+    perm = run.segs.perm.cpu().numpy()
+    skipped = perm[:L]
+    rest = np.setdiff1d(np.arange(w.T), skipped)
+    assert (y[skipped] == w.y_base[skipped]).all()
+    assert (y[rest] == y_ref[rest]).all()
+    give_ups, n_skipped = run.ws.counters()
+    assert give_ups == 0 and n_skipped == L
