@@ -390,13 +390,17 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
 // tiles (with one slice) to one XCD, so that its slice of A_i is fetched from
 // HBM once and then hit in that XCD's L2, cut the prefill shrink's HBM reads
 // by 30% but not its time, and made the ragged workload 1.5 us slower.
-__device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, SliceKind kind,
-                                          int i, Tile& t, int& my_tok, int& slice) {
+__device__ __forceinline__ int item_slot(const Plan& p, SliceKind kind, int i, int& slice) {
   const int per = 8 * (kind == kRowSlices ? p.KS : p.JS);
   const int q = i / per, rem = i - q * per;
-  const int u = 8 * q + (rem & 7);
-  t.bad = false;
   slice = rem >> 3;
+  return 8 * q + (rem & 7);
+}
+
+__device__ __forceinline__ bool item_tile(const ApplyArgs& g, const Plan& p, SliceKind kind,
+                                          int i, Tile& t, int& my_tok, int& slice) {
+  const int u = item_slot(p, kind, i, slice);
+  t.bad = false;
   if (u >= p.n_tiles) return false;
   if (!load_tile(g, u, t, my_tok)) return false;
   if (kind == kRowSlices) {
@@ -2079,42 +2083,51 @@ __device__ __forceinline__ float sum_parts(const ApplyArgs& g, const Plan& p, co
   return v;
 }
 
-// The tile's v into sm.vs, each entry summed from the partials as sum_parts
+// The expand launch's v: each entry summed from the partials as sum_parts
 // sums it (slice order, the same bits), with the loads of kSumBatch entries
 // per thread (every slice of each) issued before any is added, so that a
 // tile costs one memory round trip per batch rather than one per entry
-// (p.KS <= kMaxSlices: the host gives a tile at most 8 slices of h_in).
+// (KS <= kMaxSlices: the host gives a tile at most 8 slices of h_in).  The
+// first batch is requested as soon as the tile record is in, before the
+// rank is: entries o = l max_rank + c of the tile's rows (all max_rank
+// columns of each, whole rows of the partial-sum array), so that it travels
+// with the adapter metadata rather than after it; columns at or above the
+// tile's rank are never used.
 constexpr int kSumBatch = 4;
-__device__ __forceinline__ void sum_parts_tile(const ApplyArgs& g, const Plan& p, const Tile& t,
-                                               const Smem& sm) {
-  const int n = t.L * t.r;
+struct PartBatch {
+  float v[kSumBatch][kMaxSlices];
+};
+
+__device__ __forceinline__ void parts_issue(const ApplyArgs& g, int KS, int p0, int L, int o0,
+                                            PartBatch& pb) {
+  const int n = L * g.max_rank;
   const int64_t step = (int64_t)g.T * g.max_rank;
-  for (int o0 = 0; o0 < n; o0 += kSumBatch * kNT) {
-    float part[kSumBatch][kMaxSlices];
+  const float* base = g.vpart + (int64_t)p0 * g.max_rank;
 #pragma unroll
-    for (int i = 0; i < kSumBatch; ++i) {
-      const int o = o0 + i * kNT + threadIdx.x;
-      const int l = o < n ? o / t.r : 0, c = o < n ? o - l * t.r : 0;
-      const float* src = g.vpart + (int64_t)(t.p0 + l) * g.max_rank + c;
+  for (int i = 0; i < kSumBatch; ++i) {
+    const int o = o0 + i * kNT + threadIdx.x;
+    const float* src = base + (o < n ? o : 0);
 #pragma unroll
-      for (int ks = 0; ks < kMaxSlices; ++ks)
-        part[i][ks] = o < n && ks < p.KS ? src[ks * step] : 0.f;
-    }
-#pragma unroll
-    for (int i = 0; i < kSumBatch; ++i) {
-      const int o = o0 + i * kNT + threadIdx.x;
-      if (o < n) {
-        const int l = o / t.r, c = o - l * t.r;
-        float v = part[i][0];
-#pragma unroll
-        for (int ks = 1; ks < kMaxSlices; ++ks)
-          if (ks < p.KS) v += part[i][ks];
-        sm.vs[c * kTT + l] = v;
-      }
-    }
+    for (int ks = 0; ks < kMaxSlices; ++ks) pb.v[i][ks] = o < n && ks < KS ? src[ks * step] : 0.f;
   }
 }
 
+__device__ __forceinline__ void parts_finish(const ApplyArgs& g, int KS, const Tile& t, int o0,
+                                             const PartBatch& pb, const Smem& sm) {
+  const int n = t.L * g.max_rank;
+#pragma unroll
+  for (int i = 0; i < kSumBatch; ++i) {
+    const int o = o0 + i * kNT + threadIdx.x;
+    const int l = o / g.max_rank, c = o - l * g.max_rank;
+    if (o < n && c < t.r) {
+      float v = pb.v[i][0];
+#pragma unroll
+      for (int ks = 1; ks < kMaxSlices; ++ks)
+        if (ks < KS) v += pb.v[i][ks];
+      sm.vs[c * kTT + l] = v;
+    }
+  }
+}
 // Expand launch: item (tile, y column slice) takes the tile's v from the
 // workspace partials (plora_apply) or from g.v (plora_expand) and expands it.
 template <bool FROM_PARTS>
@@ -2124,17 +2137,40 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
   Tile t;
   int my_tok, js;
   if ((int)blockIdx.x >= p.n_items) return;
+  if (FROM_PARTS) {
+    // the tile record, then the partials' first batch together with the
+    // adapter metadata (two memory trips where three followed one another)
+    const int u = item_slot(p, kColSlices, blockIdx.x, js);
+    t.bad = false;
+    if (u >= p.n_tiles || u >= g.tile_cap) return;
+    const int4 ti = g.tiles[u];
+    t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
+    if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T) return;
+    PartBatch pb;
+    parts_issue(g, p.KS, t.p0, t.L, 0, pb);
+    my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
+    if (!tile_adapter(g, t, my_tok)) {
+      count_skipped(g, t, js);
+      return;
+    }
+    t.j0 = js * p.W;
+    t.j1 = min(g.h_out, t.j0 + p.W);
+    const Smem sm = tile_prologue(g, my_tok, apply_lds);
+    parts_finish(g, p.KS, t, 0, pb, sm);
+    for (int o0 = kSumBatch * kNT; o0 < t.L * g.max_rank; o0 += kSumBatch * kNT) {
+      parts_issue(g, p.KS, t.p0, t.L, o0, pb);
+      parts_finish(g, p.KS, t, o0, pb, sm);
+    }
+    lds_sync();
+    tile_dispatch(g, t, sm, false, true);
+    return;
+  }
   if (!item_tile(g, p, kColSlices, blockIdx.x, t, my_tok, js)) {
     count_skipped(g, t, js);
     return;
   }
   const Smem sm = tile_prologue(g, my_tok, apply_lds);
-  // (issuing the expand's first B_i and y loads before these, so that the
-  // three travel together, measured 3 us slower on the prefill workload and
-  // 1.5 us on the ragged one)
-  if (FROM_PARTS) {
-    sum_parts_tile(g, p, t, sm);
-  } else {
+  {
     for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
       const int l = o / t.r, c = o - l * t.r;
       const int tk = sm.tok[l];
