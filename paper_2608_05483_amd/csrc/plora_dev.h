@@ -1693,6 +1693,26 @@ __device__ __forceinline__ void tile_exchange(const ApplyArgs& g, const Tile& t,
   else valu_tile(g, t, sm, true, true, true, hook);
 }
 
+// tile_exchange for the one-launch forms, whose tiles have at most
+// kSmallTile tokens: only the vector paths (the same ones tile_exchange
+// takes for such tiles), so the matrix-path code and its registers stay out
+// of those kernels.
+template <class H>
+__device__ __forceinline__ void tile_exchange_small(const ApplyArgs& g, const Tile& t,
+                                                    const Smem& sm, H&& hook) {
+  static_assert(kSmallTile <= 2 && kSmallTile <= 4, "the vector paths take these tiles");
+  if (t.r & 7) {
+    shrink_gen<8>(g, t, sm);
+    hook();
+    if (t.L == 1) valu_tile_tg<1>(g, t, sm, false, true, false, NoHook{});
+    else valu_tile_tg<2>(g, t, sm, false, true, false, NoHook{});
+  } else if (t.L == 1) {
+    valu_tile_tg<1>(g, t, sm, true, true, true, hook);
+  } else {
+    valu_tile_tg<2>(g, t, sm, true, true, true, hook);
+  }
+}
+
 // Common prologue: token indices to LDS, v zeroed.
 __device__ __forceinline__ Smem tile_prologue(const ApplyArgs& g, int my_tok, void* lds) {
   Smem sm = carve(lds, g.max_rank);
@@ -1805,7 +1825,7 @@ __device__ __forceinline__ void apply_item(const ApplyArgs& g, int s, int slot, 
     t.j1 = min(g.h_out, t.j0 + W);
     const Xchg xc{sl, S, KR, (uint32_t)(stash.ep + 1),
                   g.xw + (int64_t)uni(stash.u) * kSlotWords, g.polls};
-    tile_exchange(g, t, sm, [&] {
+    tile_exchange_small(g, t, sm, [&] {
       if (!exchange_v(t, sm, xc)) {
         bump(g, 0, 1);
         plain_v(g, t, sm);
