@@ -693,15 +693,21 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
       }
     }
     lds_sync();
-    // the next batch is requested before the prefetched chunks are consumed,
-    // so that two batches are always in flight
-    uint4 a0[kCH], a1[kCH];
+    if (nj_max <= AP) {
+      // the window's chunks all came with the prefetch (a decode slice):
+      // no further batch is requested, not even a masked one (each masked
+      // load still takes address cycles ahead of the real ones)
 #pragma unroll
-    for (int j = 0; j < kCH; ++j)
-      a0[j] = bld16(ra, ae + (AP + j) * astep, oct_ok && AP + j < nj);
+      for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
+    } else {
+      // the next batch is requested before the prefetched chunks are
+      // consumed, so that two batches are always in flight
+      uint4 a0[kCH], a1[kCH];
 #pragma unroll
-    for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
-    if (nj_max > AP) {
+      for (int j = 0; j < kCH; ++j)
+        a0[j] = bld16(ra, ae + (AP + j) * astep, oct_ok && AP + j < nj);
+#pragma unroll
+      for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
       for (int jb = AP; jb < nj_max; jb += 2 * kCH) {
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
