@@ -1,6 +1,8 @@
 // k_apply.hip -- plora_apply as one launch with the slice exchange.
 // every adapter byte is read once per call here: non-temporal reads
 #define PLORA_ADAPTER_POLICY 2
+// decode-sized slices: a prefetch of 4 chunks covers them
+#define PLORA_PREFETCH_CHUNKS 4
 #include "plora_dev.h"
 
 namespace plora_impl {

@@ -211,13 +211,18 @@ constexpr int kNT = 256;             // threads per work group
 constexpr int kW = kNT / 64;         // wavefronts per work group
 constexpr int kWGPerCU = 2;          // resident work groups per compute unit
 // Chunks of A_i and of B_i per thread requested up front by the vector path
-// (one batch of kCH; the rest follow in batches).  A decode item needs 4 of
-// each; with 16 (8 of B at two tokens), the masked slots still cost address
-// cycles ahead of the real ones: 8 measured decode 14.3 -> 13.7 us per
-// launch, ragged 62.9 -> 61.8, prefill 78.5 -> 77.8, the large batch
-// 49.7 -> 50.0.
-constexpr int kAP = 8;
-constexpr int kBP = 8;
+// (the rest follow in batches of kCH).  A decode item needs 4 of each, and a
+// masked slot still costs address cycles ahead of the real ones: the
+// one-launch forms (decode-sized slices) request 4 (decode 14.3 us per
+// launch with 16, 13.6 with 8, 13.15 with 4; the large batch 49.7, 50.1,
+// 49.5), the two-launch forms 8 (ragged 62.9 with 16, 62.1 with 8, 62.8 with
+// 4).  A kernel file sets PLORA_PREFETCH_CHUNKS before including this header.
+#ifndef PLORA_PREFETCH_CHUNKS
+#define PLORA_PREFETCH_CHUNKS 8
+#endif
+constexpr int kAP = PLORA_PREFETCH_CHUNKS;
+constexpr int kBP = PLORA_PREFETCH_CHUNKS;
+static_assert(kAP <= kCH || kAP % kCH == 0, "whole batches, or one short one");
 constexpr int kXW = 4096;            // x row window staged in LDS (vector path)
 constexpr int kChunk = 16384;        // bf16 elements per LDS staging chunk (32 KiB)
 constexpr int kWaveRing = 12288;     // bytes of LDS ring per wavefront (matrix shrink)
@@ -606,11 +611,11 @@ __device__ __forceinline__ void x_row(const uint16_t* xs, int row, float (&xf)[T
 
 // acc[tt][e] += x[tt][row] * A[row][oct*8 + e] for chunks jb..jb+kCH-1 of the
 // window starting at chunk q0 (rows relative to w0).
-template <int R_OCT, int TG>
+template <int R_OCT, int TG, int N = kCH>
 __device__ __forceinline__ void fma_a(float (&val)[TG * 8], const uint4* a, const uint16_t* xs,
                                       int q0, int w0, int jb, int nj) {
 #pragma unroll
-  for (int j = 0; j < kCH; ++j) {
+  for (int j = 0; j < N; ++j) {
     if (jb + j < nj) {
       const int row = (q0 + (int)threadIdx.x + (jb + j) * kNT) / R_OCT - w0;
       float xf[TG];
@@ -698,7 +703,8 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
       // no further batch is requested, not even a masked one (each masked
       // load still takes address cycles ahead of the real ones)
 #pragma unroll
-      for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
+      for (int jb = 0; jb < AP; jb += kCH)
+        fma_a<R_OCT, TG, (AP < kCH ? AP : kCH)>(val, apre + jb, xs, q0, w0, jb, nj);
     } else {
       // the next batch is requested before the prefetched chunks are
       // consumed, so that two batches are always in flight
@@ -707,7 +713,8 @@ __device__ __forceinline__ void shrink_valu(const ApplyArgs& g, const Tile& t, c
       for (int j = 0; j < kCH; ++j)
         a0[j] = bld16(ra, ae + (AP + j) * astep, oct_ok && AP + j < nj);
 #pragma unroll
-      for (int jb = 0; jb < AP; jb += kCH) fma_a<R_OCT, TG>(val, apre + jb, xs, q0, w0, jb, nj);
+      for (int jb = 0; jb < AP; jb += kCH)
+        fma_a<R_OCT, TG, (AP < kCH ? AP : kCH)>(val, apre + jb, xs, q0, w0, jb, nj);
       for (int jb = AP; jb < nj_max; jb += 2 * kCH) {
 #pragma unroll
         for (int j = 0; j < kCH; ++j)
@@ -762,11 +769,11 @@ __device__ __forceinline__ void v_row(const float* vs, int c, float (&vf)[TG]) {
 
 // d[tt][e] += v[tt][row] * B_i[row][co*8 + e] for this thread's rows
 // jb..jb+kCH-1.
-template <int TG>
+template <int TG, int N = kCH>
 __device__ __forceinline__ void fma_b(float (&d)[TG * 8], const uint4* b, const Smem& sm,
                                       const ExpandMap& m, int jb) {
 #pragma unroll
-  for (int j = 0; j < kCH; ++j) {
+  for (int j = 0; j < N; ++j) {
     if (jb + j < m.njb) {
       float vf[TG];
       v_row<TG>(sm.vs, m.rb + (jb + j) * m.RSB, vf);
@@ -803,7 +810,7 @@ __device__ __forceinline__ void expand_valu(const ApplyArgs& g, const Tile& t, c
       int jb0 = 0;
       if (cb == 0) {
 #pragma unroll
-        for (int jb = 0; jb < BP; jb += kCH) fma_b<TG>(d, bpre + jb, sm, m, jb);
+        for (int jb = 0; jb < BP; jb += kCH) fma_b<TG, (BP < kCH ? BP : kCH)>(d, bpre + jb, sm, m, jb);
         jb0 = BP;
       }
       // the remaining rows in batches of kCH, the next batch always requested
