@@ -3,6 +3,7 @@
 #define PLORA_ADAPTER_POLICY 2
 // decode-sized slices: a prefetch of 4 chunks covers them
 #define PLORA_PREFETCH_CHUNKS 4
+#define PLORA_X_WINDOW 2048
 #include "plora_dev.h"
 
 namespace plora_impl {

@@ -223,7 +223,14 @@ constexpr int kWGPerCU = 2;          // resident work groups per compute unit
 constexpr int kAP = PLORA_PREFETCH_CHUNKS;
 constexpr int kBP = PLORA_PREFETCH_CHUNKS;
 static_assert(kAP <= kCH || kAP % kCH == 0, "whole batches, or one short one");
-constexpr int kXW = 4096;            // x row window staged in LDS (vector path)
+// Columns of x staged in LDS per window by the vector path (and shrink_gen).
+// A decode slice is 512 columns, which a 2048-column window stages without
+// masked slots at one token per tile; a kernel file may set
+// PLORA_X_WINDOW before including this header.
+#ifndef PLORA_X_WINDOW
+#define PLORA_X_WINDOW 4096
+#endif
+constexpr int kXW = PLORA_X_WINDOW;
 constexpr int kChunk = 16384;        // bf16 elements per LDS staging chunk (32 KiB)
 constexpr int kWaveRing = 12288;     // bytes of LDS ring per wavefront (matrix shrink)
 constexpr int kBufElems = kW * kWaveRing / 2 + 16;   // slack for transposed reads past the end
