@@ -213,6 +213,13 @@ def _seg_inputs():
         idx = rng.integers(-1, N, size=T).astype(np.int32)
         cases.append((f"rand_T{T}_N{N}", idx, N))
     cases.append(("zipf_max", W.zipf_ids(rng, 16384, 1000, 1.0), 1000))
+    # the counting sort's degenerate batches: nothing valid, nothing but
+    # out-of-range ids, one id for every token, and chunks of one id each
+    cases.append(("all_none_T300", np.full(300, -1, np.int32), 7))
+    cases.append(("all_invalid_T600", rng.integers(50, 1 << 30, size=600).astype(np.int32), 50))
+    cases.append(("one_id_T5000", np.full(5000, 3, np.int32), 4))
+    cases.append(("runs_of_64_T4096", np.repeat(rng.integers(0, 2047, size=64), 64).astype(np.int32),
+                  2047))
     return cases
 
 
