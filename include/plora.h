@@ -200,21 +200,24 @@ typedef struct {
 int32_t plora_tile_capacity(int32_t T, int32_t n_adapters);
 
 /* Host.  Bytes of device workspace plora_apply and plora_shrink need for a
- * batch of up to T tokens over this adapter stack; 0 for T <= 0.  Three
+ * batch of up to T tokens over this adapter stack; 0 for T <= 0.  Four
  * sections, each starting on a 256-byte boundary:
  *   1. the epochs of the one-launch apply's tile slots: 336 64-bit words,
  *      then two 64-bit counters (see plora_workspace_counters);
- *   2. its exchange regions: 8 * PLORA_SMALL_BATCH_TILE_TOKENS * 128
- *      64-bit words (16 KiB) for each of P = min(336, max(8, cap8)) tile
- *      slots, cap8 being plora_tile_capacity(T, N) rounded up to a
- *      multiple of 8;
- *   3. the partial sums of v over up to 8 slices of h_in, fp32,
+ *   2. the readiness words of the one-launch form above 256 tokens: 4096
+ *      64-bit words, one per tile slot;
+ *   3. the exchange regions of the one-launch form up to 256 tokens:
+ *      8 * PLORA_SMALL_BATCH_TILE_TOKENS * 128 64-bit words (16 KiB) for each
+ *      of P = min(336, max(8, cap8)) tile slots, cap8 being
+ *      plora_tile_capacity(T, N) rounded up to a multiple of 8;
+ *   4. the partial sums of v over up to 8 slices of h_in, fp32,
  *      K * T * max_rank * 4 bytes with K = min(8, max(1, h_in / 512)).
- * Sections 1 and 2 keep their offsets whatever T, the ranks or the slice
+ * Sections 1 to 3 keep their offsets whatever T, the ranks or the slice
  * count, so one workspace serves calls of any batch size up to T and any
  * adapter stack it is large enough for.  Zero it once with
  * plora_workspace_init before its first use; afterwards it carries the
- * epochs from call to call and must not be written by the caller.  Calls
+ * epochs and readiness words from call to call (every call leaves the
+ * readiness words at zero) and must not be written by the caller.  Calls
  * that share one must not overlap in time.  plora_segment and plora_expand
  * take none (ws may be NULL). */
 size_t plora_workspace_bytes(int32_t T, const plora_adapters* ad);
@@ -269,16 +272,19 @@ plora_status plora_expand(const float* v, int64_t ldv,
 
 /*
  * The apply: y[t] = bf16(y[t] + s_i (x[t] A_i) B_i) for every valid token
- * (strategy E1: both matrices resident in GPU memory, section V-A).  For
- * T <= 256 one launch; above, two launches with v's partial sums passed
- * through ws.  ws must hold plora_workspace_bytes(T) bytes, 16-byte aligned,
- * zeroed once by plora_workspace_init before its first use, in both cases.
- * When a batch has few tiles (the decode case), each tile is reduced by up
- * to 8 work groups of the launch, which trade their partial sums of v
- * through ws; a work group never waits for another without bound: if a
- * partner does not publish within a bounded number of polls (it was not
- * scheduled), the work group computes v by itself, which is correct to fp32
- * accuracy but summed in another order.  Apart from that case the result is
+ * (strategy E1: both matrices resident in GPU memory, section V-A).  One
+ * launch: for T <= 256 with each tile split over up to 8 work groups, which
+ * trade their partial sums of v through ws; above, with the shrink work
+ * groups (one per tile and slice of h_in) storing partial sums of v in ws,
+ * and the expand work groups (one per tile and slice of y's columns)
+ * starting on a tile once its partial sums are stored.  A batch whose tile
+ * capacity exceeds 4096 takes two launches, the shrink's and the expand's.
+ * ws must hold plora_workspace_bytes(T) bytes, 16-byte aligned, zeroed once
+ * by plora_workspace_init before its first use, in every case.  A work
+ * group never waits for another without bound: if a partner does not
+ * publish within a bounded number of polls (it was not scheduled), the work
+ * group computes v by itself, which is correct to fp32 accuracy but summed
+ * in another order.  Apart from that case the result is
  * bit for bit the same as plora_shrink followed by plora_expand, and
  * bitwise deterministic.  x and y must not overlap.
  */
@@ -327,7 +333,8 @@ plora_status plora_segment_apply_noalloc(const int32_t* idx, const uint16_t* x, 
 
 /* Host.  How many launches plora_segment_apply makes for a batch of T
  * tokens over this stack: 1 (the one-launch form), 2 (plora_segment then
- * a one-launch plora_apply) or 3 (then a two-launch one); 0 for T <= 0 or
+ * a one-launch plora_apply) or 3 (then a two-launch one, for a tile
+ * capacity above 4096); 0 for T <= 0 or
  * a stack plora_apply would reject. */
 int32_t plora_segment_apply_launches(int32_t T, const plora_adapters* ad);
 
@@ -386,8 +393,9 @@ plora_status plora_pool_device_pointer(const void* host, const void** device);
 /* Host, synchronous (copies two words and waits on stream).  The counters
  * a workspace keeps since plora_workspace_init zeroed it, summed over every
  * call made with it:
- *   counts[0]  one-launch work items whose exchange partners did not publish
- *              in time, so that they computed v alone (their calls' bits can
+ *   counts[0]  one-launch work items whose partners (the tile's other
+ *              slices, or above 256 tokens its shrink work groups) did not
+ *              publish in time, so that they computed v alone (their calls' bits can
  *              differ in the last places; see plora_apply);
  *   counts[1]  tokens that kept y_base because their adapter entry breaks
  *              the contract (a rank outside [0, max_rank], or a block

@@ -111,15 +111,17 @@ int fused_slices(int32_t tile_cap, int32_t h_in, int32_t h_out, int32_t max_rank
 }
 
 // Workspace sections, each 256-byte aligned: the epochs of the exchange's
-// tile slots (64-bit, kXSlots of them), the exchange regions of the
+// tile slots (64-bit, kXSlots of them) and the counters; the readiness words
+// of the one-launch two-part form (kReadyTiles); the exchange regions of the
 // one-launch form (kSlotWords 64-bit words for each of the first
-// min(cap8, kXSlots) tile slots), then the partial sums of v of the
-// two-launch form and plora_shrink (fp32 [ks_max][T][max_rank]).  The
-// epochs and each slot's region sit at the same offsets for every batch
-// size, rank and slice count, which the tags rely on; only the last
-// section's place and size follow the shapes.
+// min(cap8, kXSlots) tile slots); then the partial sums of v of the
+// two-part forms and plora_shrink (fp32 [ks_max][T][max_rank]).  The epochs,
+// the readiness words and each slot's region sit at the same offsets for
+// every batch size, rank and slice count, which their tags rely on (no
+// other section ever writes there); only the last section's place and size
+// follow the shapes.
 struct WsLayout {
-  size_t xep, counters, xw, vpart, total;
+  size_t xep, counters, ready, xw, vpart, total;
 };
 
 // Workspace bytes of the multi-work-group segmentation (batches above 1024
@@ -134,13 +136,16 @@ size_t segment_scratch_bytes(int32_t T, int32_t N) {
 }
 
 constexpr int kCounters = 2;   // workspace counters after the epochs (see ApplyArgs)
+// Readiness words of the one-launch two-part form (one per tile slot); a
+// batch whose tile capacity exceeds it takes two launches.
+constexpr int32_t kReadyTiles = 4096;
 
 constexpr size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // n adapter stacks (the projections of plora_apply_multi; n = 1 otherwise)
 // sharing the batch: n cap8 tile slots, and the largest partial-sum section.
 WsLayout ws_layout(int32_t T, const plora_adapters* ad, int n = 1) {
-  WsLayout l{0, 0, 0, 0, 0};
+  WsLayout l{0, 0, 0, 0, 0, 0};
   if (!ad || T <= 0 || n < 1) return l;
   size_t nvp = 0;
   for (int p = 0; p < n; ++p) {
@@ -154,7 +159,8 @@ WsLayout ws_layout(int32_t T, const plora_adapters* ad, int n = 1) {
   const size_t slots = (size_t)std::min(kXSlots, std::max(8, n * ((tcap + 7) & ~7)));
   l.xep = 0;
   l.counters = (size_t)kXSlots * sizeof(uint64_t);
-  l.xw = align256(l.counters + kCounters * sizeof(uint64_t));
+  l.ready = align256(l.counters + kCounters * sizeof(uint64_t));
+  l.xw = align256(l.ready + kReadyTiles * sizeof(uint64_t));
   l.vpart = align256(l.xw + slots * kSlotWords * sizeof(uint64_t));
   l.total = align256(l.vpart + nvp);
   return l;
@@ -258,6 +264,7 @@ plora_status prepare(const plora_adapters* ad, const plora_segments* seg, void* 
     g.xw = reinterpret_cast<uint64_t*>(base + l.xw);
     g.xep = reinterpret_cast<uint64_t*>(base + l.xep);
     g.counters = reinterpret_cast<unsigned long long*>(base + l.counters);
+    g.ready = reinterpret_cast<uint64_t*>(base + l.ready);
   } else if (ws && aligned16(ws) && ws_bytes >= ws_layout(1, ad).xw) {
     // a call that needs no workspace still counts into one it is given
     g.counters = reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(ws) +
@@ -295,10 +302,11 @@ plora_status launch_items(ItemLauncher launch, const ApplyArgs& g, int s_max,
 // Largest batch plora_segment_apply_noalloc takes, and the workspace such a
 // batch needs at most: the exchange regions of min(kXSlots, cap8) tile
 // slots (cap8 <= kNoAllocTokens) and the partial sums of v for up to 8
-// slices of h_in at rank 128, after the epochs and counters.
+// slices of h_in at rank 128, after the epochs, counters and readiness words.
 constexpr int32_t kNoAllocTokens = 256;
 constexpr size_t kScratchBytes =
-    align256(align256(align256((size_t)(kXSlots + kCounters) * sizeof(uint64_t)) +
+    align256(align256(align256(align256((size_t)(kXSlots + kCounters) * sizeof(uint64_t)) +
+                               (size_t)kReadyTiles * sizeof(uint64_t)) +
                       (size_t)std::min(kXSlots, kNoAllocTokens) * kSlotWords * sizeof(uint64_t)) +
              (size_t)8 * kNoAllocTokens * PLORA_MAX_RANK * sizeof(float));
 
@@ -446,6 +454,12 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx, const plora_adapters* a
   if (g.fixed_slices > 1) return launch_items(launch_apply, g, g.js_max, stream);
   if (fused_for(seg->T))
     return launch_items(launch_apply_cols, g, g.js_max, stream);
+  if (g.tile_cap <= kReadyTiles) {
+    clear_stale_error();
+    launch_parts(g, grid_for(g, g.ks_max), grid_for(g, g.js_max),
+                 smem_bytes(g.h_in, g.max_rank), stream);
+    return launch_status();
+  }
   ApplyArgs gs = g;
   gs.count_skips = 0;                 // the expand launch counts the call's skips
   st = launch_items(launch_shrink_part, gs, g.ks_max, stream);
@@ -478,7 +492,7 @@ plora_status plora_segment_apply_noalloc(const int32_t* idx, const uint16_t* x, 
 int32_t plora_segment_apply_launches(int32_t T, const plora_adapters* ad) {
   if (T <= 0 || !ad || check_adapters_host(ad) != PLORA_OK) return 0;
   if (segment_apply_one_launch(T, ad)) return 1;
-  return fused_for(T) ? 2 : 3;
+  return fused_for(T) || plora_tile_capacity(T, ad->n_adapters) <= kReadyTiles ? 2 : 3;
 }
 
 plora_status plora_segment_apply(const int32_t* idx, const uint16_t* x, int64_t ldx,

@@ -282,6 +282,9 @@ struct ApplyArgs {
   // computed v alone, [1] tokens skipped for an unusable adapter entry
   unsigned long long* counters;
   int32_t count_skips;  // this launch counts skipped tokens (one launch per call does)
+  // the one-launch two-part form (see parts_kernel): a readiness word per
+  // tile slot
+  uint64_t* ready;
 };
 
 struct Tile {
@@ -2144,6 +2147,8 @@ struct PartBatch {
   float v[kSumBatch][kMaxSlices];
 };
 
+// (COH: loads at agent scope, for partials stored earlier in the same launch)
+template <bool COH = false>
 __device__ __forceinline__ void parts_issue(const ApplyArgs& g, int KS, int p0, int L, int o0,
                                             PartBatch& pb) {
   const int n = L * g.max_rank;
@@ -2154,7 +2159,14 @@ __device__ __forceinline__ void parts_issue(const ApplyArgs& g, int KS, int p0, 
     const int o = o0 + i * kNT + threadIdx.x;
     const float* src = base + (o < n ? o : 0);
 #pragma unroll
-    for (int ks = 0; ks < kMaxSlices; ++ks) pb.v[i][ks] = o < n && ks < KS ? src[ks * step] : 0.f;
+    for (int ks = 0; ks < kMaxSlices; ++ks) {
+      if constexpr (COH)
+        pb.v[i][ks] = o < n && ks < KS ? __hip_atomic_load(src + ks * step, __ATOMIC_RELAXED,
+                                                           __HIP_MEMORY_SCOPE_AGENT)
+                                       : 0.f;
+      else
+        pb.v[i][ks] = o < n && ks < KS ? src[ks * step] : 0.f;
+    }
   }
 }
 
@@ -2227,6 +2239,125 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
   tile_dispatch(g, t, sm, false, true);
 }
 
+// ---------------------------------------------------------------------------
+// the two parts in one launch
+// ---------------------------------------------------------------------------
+//
+// Batches above kFusedTokens tokens: the shrink items (tile, h_in slice) and
+// the expand items (tile, column slice) of the two-launch form run as one
+// launch, the expand items after every shrink item in the grid.  An expand
+// item starts on its tile as soon as that tile's KS partials are stored,
+// rather than after the last shrink item of the launch, so the expand items
+// fill the compute units the shrink's tail leaves idle, and the gap between
+// two launches goes.
+//
+// Each tile slot has a readiness word that counts the tile's items: a shrink
+// item adds 1 once its partials are stored, an expand item adds 256 once it
+// has seen all KS shrink additions (or given up waiting), and the item whose
+// addition completes the count KS + 256 JS sets the word back to 0.  So the
+// word is 0 when a call starts, however the previous call went (an expand
+// item that gave up still adds, and a shrink item that comes after it still
+// completes the count), and the low byte reaches KS only through this
+// call's shrink items.  No word is shared by all work groups (one address
+// taking an atomic from each of about 2700 work groups measured 80 us).
+//  - A shrink item stores its partials at agent scope (sc1: the L2 writes
+//    them through to memory), waits until each thread's stores are
+//    acknowledged (vmcnt counts stores), and after a work-group barrier adds
+//    its 1.  (An agent-scope release fence, buffer_wbl2, would write back
+//    the whole L2: it measured 30 us per call.)
+//  - An expand item polls the word until its low byte is KS, then reads the
+//    partials at agent scope, so that no stale line in its L1 or L2 answers.
+// Progress: the shrink items come before every expand item in the grid, and
+// each XCD dispatches its work groups in index order, so a shrink item that
+// an expand item waits for is queued on its own XCD behind shrink items
+// only, which never wait: it is bound to run.  The wait is bounded all the
+// same: an item that gives up computes v over all of h_in by itself
+// (plain_v, counted like an exchange give-up), and the call's bits can then
+// differ in the last places.
+
+constexpr unsigned long long kExpandCount = 256;   // an expand item's addition
+
+__device__ __forceinline__ unsigned long long parts_total(const Plan& p) {
+  return (unsigned long long)p.KS + kExpandCount * (unsigned long long)p.JS;
+}
+
+// Adds n to tile u's readiness word (thread 0); the addition that completes
+// the tile's count clears the word for the next call.
+__device__ __forceinline__ void ready_add(const ApplyArgs& g, const Plan& p, int u,
+                                          unsigned long long n) {
+  const unsigned long long old =
+      __hip_atomic_fetch_add(g.ready + u, (uint64_t)n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (old + n == parts_total(p))
+    __hip_atomic_store(g.ready + u, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Shrink item i (as shrink_part_kernel), then its addition to the tile's word.
+__device__ __forceinline__ void parts_shrink_item(const ApplyArgs& g, int i, unsigned char* lds) {
+  const Plan p = make_plan(g, kRowSlices);
+  if (i >= p.n_items) return;
+  int ks;
+  const int u = item_slot(p, kRowSlices, i, ks);
+  if (u >= p.n_tiles) return;
+  Tile t;
+  int my_tok;
+  if (item_tile(g, p, kRowSlices, i, t, my_tok, ks)) {
+    const Smem sm = tile_prologue(g, my_tok, lds);
+    tile_dispatch(g, t, sm, true, false);
+    float* dst = g.vpart + ((int64_t)ks * g.T + t.p0) * g.max_rank;
+    for (int o = threadIdx.x; o < t.L * t.r; o += kNT) {
+      const int l = o / t.r, c = o - l * t.r;
+      __hip_atomic_store(dst + l * g.max_rank + c, sm.vs[c * kTT + l], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  // (tokens of an unusable entry are counted by the expand items)
+  wait_vm<0>();
+  lds_sync();
+  if (threadIdx.x == 0) ready_add(g, p, u, 1);
+}
+
+// Expand item i (as expand_kernel<true>), once its tile's partials are in.
+__device__ __forceinline__ void parts_expand_item(const ApplyArgs& g, int i, unsigned char* lds,
+                                                  int* ok_sh) {
+  const Plan p = make_plan(g, kColSlices);
+  if (i >= p.n_items) return;
+  int js;
+  const int u = item_slot(p, kColSlices, i, js);
+  if (u >= p.n_tiles) return;
+  Tile t;
+  t.bad = false;
+  int my_tok;
+  if (!load_tile(g, u, t, my_tok)) {
+    count_skipped(g, t, js);
+    if (threadIdx.x == 0) ready_add(g, p, u, kExpandCount);
+    return;
+  }
+  t.j0 = js * p.W;
+  t.j1 = min(g.h_out, t.j0 + p.W);
+  if (threadIdx.x == 0) {
+    unsigned long long w = xload(g.ready + u);
+    for (int it = 0; (w & 255) != (unsigned)p.KS && it < g.polls; ++it) {
+      __builtin_amdgcn_s_sleep(2);
+      w = xload(g.ready + u);
+    }
+    *ok_sh = (w & 255) == (unsigned)p.KS;
+    ready_add(g, p, u, kExpandCount);
+  }
+  const Smem sm = tile_prologue(g, my_tok, lds);     // ends with a barrier
+  if (*ok_sh) {
+    PartBatch pb;
+    for (int o0 = 0; o0 < t.L * g.max_rank; o0 += kSumBatch * kNT) {
+      parts_issue<true>(g, p.KS, t.p0, t.L, o0, pb);
+      parts_finish(g, p.KS, t, o0, pb, sm);
+    }
+  } else {
+    bump(g, 0, 1);
+    plain_v(g, t, sm);
+  }
+  lds_sync();
+  tile_dispatch(g, t, sm, false, true);
+}
+
 // Dynamic LDS above 64 KB is opted into once per kernel.
 inline void allow_lds(const void* kernel, std::atomic<bool>& done) {
   if (done.load()) return;
@@ -2249,6 +2380,8 @@ void launch_segment_groups(const int32_t* idx, int32_t T, int32_t N, int32_t cap
                            int32_t* meta, int4* tiles, int32_t* table, hipStream_t stream);
 void launch_zero(uint4* p, size_t n16, unsigned blocks, hipStream_t stream);
 void launch_shrink_part(const ApplyArgs& g, unsigned grid, size_t lds, hipStream_t stream);
+void launch_parts(const ApplyArgs& g, unsigned n_shrink, unsigned n_expand, size_t lds,
+                  hipStream_t stream);
 void launch_gather_v(const ApplyArgs& g, unsigned grid, hipStream_t stream);
 void launch_apply(const ApplyArgs& g, unsigned grid, size_t lds, hipStream_t stream);
 void launch_apply_cols(const ApplyArgs& g, unsigned grid, size_t lds, hipStream_t stream);

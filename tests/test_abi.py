@@ -82,7 +82,8 @@ def _apply_status(ad=None, seg=None, x=FAKE, ldx=256, y=FAKE, ldy=256, ws=FAKE,
 
 
 def _expected_ws(T, N, h_in, max_rank):
-    """The documented layout: 336 64-bit epochs, then one exchange region of
+    """The documented layout: 336 64-bit epochs and two counters, 4096
+    readiness words (64-bit), then one exchange region of
     8 x PLORA_SMALL_BATCH_TILE_TOKENS x 128 64-bit words per tile slot for min(336, max(8, cap8)) slots
     (cap8 = the tile capacity rounded up to 8), then the partial sums of v
     over min(8, h_in / 512) slices of h_in (fp32), each section 256-byte
@@ -90,7 +91,8 @@ def _expected_ws(T, N, h_in, max_rank):
     up = lambda v: (v + 255) // 256 * 256
     k = min(8, max(1, h_in // 512))
     slots = min(336, max(8, (P.plora_tile_capacity(T, N) + 7) // 8 * 8))
-    return up(up(up(336 * 8) + slots * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8) + k * T * max_rank * 4)
+    head = up(up(336 * 8 + 2 * 8) + 4096 * 8)
+    return up(up(head + slots * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8) + k * T * max_rank * 4)
 
 
 def test_workspace_size_and_checks():
@@ -103,7 +105,7 @@ def test_workspace_size_and_checks():
     for T in (8, 64, 300, 1024, 16384):
         assert P.plora_workspace_bytes(T, big) == _expected_ws(T, 1000, 4096, 16)
     assert (P.plora_workspace_bytes(16384, big) - 8 * 16384 * 16 * 4
-            < 337 * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8 + 4096)
+            < 337 * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8 + 4096 * 8 + 4096)
     ad = _ad()
     assert P.plora_workspace_bytes(0, ad) == 0
     assert P.lib.plora_workspace_init(None, 0, None) == P.PLORA_OK
@@ -238,7 +240,7 @@ def test_apply_multi_host_checks():
     need = P.lib.plora_workspace_bytes_multi(8, arr, 2)
     up = lambda v: (v + 255) // 256 * 256
     slots = min(336, max(8, 2 * ((P.plora_tile_capacity(8, 4) + 7) // 8 * 8)))
-    assert need == up(up(up(336 * 8) + slots * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8) + 8 * 8 * 4)
+    assert need == up(up(up(up(336 * 8 + 2 * 8) + 4096 * 8) + slots * 8 * P.PLORA_SMALL_BATCH_TILE_TOKENS * 128 * 8) + 8 * 8 * 4)
     assert need >= P.plora_workspace_bytes(8, a)
     assert P.lib.plora_workspace_bytes_multi(8, arr, 0) == 0
     assert P.lib.plora_workspace_bytes_multi(8, arr, P.PLORA_MAX_PROJECTIONS + 1) == 0
@@ -346,8 +348,12 @@ def test_segment_apply_launch_count():
     assert P.plora_segment_apply_launches(1, dec) == 1
     assert P.plora_segment_apply_launches(65, dec) == 1     # the whole work group segments
     assert P.plora_segment_apply_launches(256, dec) == 1
-    assert P.plora_segment_apply_launches(257, dec) == 3    # segment, then two apply launches
-    assert P.plora_segment_apply_launches(4096, dec) == 3   # segment, then two apply launches
+    assert P.plora_segment_apply_launches(257, dec) == 2    # segment, then the two-part launch
+    assert P.plora_segment_apply_launches(4096, dec) == 2
+    # above 4096 tile slots: segment, then shrink and expand launches
+    wide = _ad(n_adapters=5000, h_in=4096, max_rank=16)
+    assert P.plora_tile_capacity(5000, 5000) > 4096
+    assert P.plora_segment_apply_launches(5000, wide) == 3
     assert P.plora_segment_apply_launches(8, _ad()) == 2    # h = 256: no split form
     assert P.plora_segment_apply_launches(0, dec) == 0
     assert P.plora_segment_apply_launches(8, _ad(h_in=12)) == 0

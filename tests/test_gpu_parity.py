@@ -378,6 +378,63 @@ def test_exchange_fallback_meets_the_bars(P):
         assert (run.apply() == run.expand(run.shrink())).all()
 
 
+def test_two_part_fallback_meets_the_bars(P):
+    """Batches above 256 tokens run their shrink and expand items in one
+    launch, each expand item polling its tile's readiness word; with polls
+    forced to 0 the items that find their tile not ready compute v by
+    themselves, which meets the oracle's bars, and the default again gives
+    the split calls' bits."""
+    w = workload("ragged", "parity")
+    say("two-part fallback ragged/parity")
+    run = Run(P, w).segment()
+    P.plora_debug_set_exchange_polls(0)
+    try:
+        y = run.apply()
+    finally:
+        P.plora_debug_set_exchange_polls(-1)
+    yref, yout = oracle_y(w)
+    check_y(y, yref, yout, w, strict_l2=True)
+    assert (run.apply() == run.expand(run.shrink())).all()
+
+
+def test_two_launches_above_the_readiness_words(P):
+    """A batch whose tile capacity exceeds the 4096 readiness words (4500
+    tokens over 4200 adapters) takes the shrink and expand launches; its
+    result meets the oracle's bars and equals the split calls' bits."""
+    rng = np.random.default_rng(12)
+    idx = rng.integers(-1, 4200, size=4500).astype(np.int32)
+    w = W.make_workload("tiny", scale="parity", idx=idx, n_adapters=4200)
+    assert P.plora_tile_capacity(4500, 4200) > 4096
+    say("two launches T=4500 N=4200")
+    run = Run(P, w).segment()
+    y = run.apply()
+    yref, yout = oracle_y(w)
+    check_y(y, yref, yout, w, strict_l2=True)
+    assert (y == run.expand(run.shrink())).all()
+
+
+def test_workspace_across_large_batches(P):
+    """One workspace serving calls above 256 tokens of varying size in turn
+    (their readiness words and epoch carry over from call to call), with
+    one-launch calls between them."""
+    w0 = workload("ragged", "parity")
+    ad = P.Adapters.from_workload(w0)
+    ws = P.Workspace(4096, ad)
+    rng = np.random.default_rng(6)
+    for k, T in enumerate((1024, 300, 64, 4096, 257, 2000, 300)):
+        idx = W.zipf_ids(rng, T, w0.n_adapters, 0.8)
+        ww = W.with_idx(w0, idx)
+        say(f"large-batch workspace call {k}: T={T}")
+        segs = P.Segments(T, w0.n_adapters)
+        P.segment(dev(idx), segs)
+        x = dev(np.ascontiguousarray(ww.x).view(np.int16))
+        y = dev(np.ascontiguousarray(ww.y_base).view(np.int16))
+        P.apply(x, ad, segs, y, ws)
+        torch.cuda.synchronize()
+        yref, yout = oracle_y(ww)
+        check_y(bits16(y), yref, yout, ww, strict_l2=True)
+
+
 def test_workspace_shared_across_batches_and_stacks(P):
     """One workspace serving one-launch calls of varying batch size and of two
     adapter stacks (ranks 16 and 64) in turn: its exchange regions and epochs
