@@ -744,7 +744,7 @@ def _segapply_cases():
         ("decode_desc", "decode", np.arange(64, dtype=np.int32)[::-1].copy() * 15),
         ("large", "large", None),
         ("tiny_two_calls", "tiny", None),
-        # above 1024 tokens: the counting-sort segmentation, then two launches
+        # above 1024 tokens: the counting-sort segmentation, then the two-part launch
         ("prefill_counting", "prefill", None),
     ]
 

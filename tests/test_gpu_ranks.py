@@ -107,16 +107,17 @@ def test_rank_matches_oracle_in_every_form(P, r):
 
 
 @pytest.mark.parametrize("r", [3, 12, 48, 100, 128])
-def test_rank_two_launch_prefill_form(P, r):
-    """Batches above 1024 tokens take the two-launch form (partial v per h_in
-    slice through the workspace), here at the prefill shape (h_in = 8192,
+def test_rank_two_part_prefill_form(P, r):
+    """Batches above 256 tokens take the two-part form (shrink work groups
+    pass partial v per h_in slice through the workspace to the expand work
+    groups, in one launch), here at the prefill shape (h_in = 8192,
     h_out = 1024) with requests of up to 300 tokens."""
     rng = np.random.default_rng(200 + r)
     N = 40
     lens = list(rng.integers(150, 300, size=8)) + [1, 2, 5, 33]
     idx = lengths_idx(rng, N, lens)
     w = W.make_workload("prefill", scale="parity", ranks=r, n_adapters=N, idx=idx)
-    say(f"rank {r} two-launch: T={w.T}")
+    say(f"rank {r} two-part: T={w.T}")
     assert w.T > 1024
     run = Run(P, w).segment()
     y = run.apply()
@@ -131,7 +132,7 @@ def test_rank_two_launch_prefill_form(P, r):
 def test_mixed_ranks_1_to_128_in_one_stack(P):
     """One stack whose adapters carry every rank from 0 to 128 side by side
     (ragged offsets), through a decode batch, a 256-token batch, a batch of
-    mixed segment lengths and a two-launch batch."""
+    mixed segment lengths and a two-part batch."""
     rng = np.random.default_rng(77)
     N = 300
     ranks = rng.integers(1, 129, size=N).astype(np.int32)
@@ -142,7 +143,7 @@ def test_mixed_ranks_1_to_128_in_one_stack(P):
     batches = [("zipf64", W.zipf_ids(rng, 64, N, 1.0)),
                ("uniform256", W.uniform_ids(rng, 256, N)),
                ("lengths", lengths_idx(rng, N, LENGTHS)),
-               ("two_launch", lengths_idx(rng, N, list(rng.integers(1, 200, size=12)) +
+               ("two_part", lengths_idx(rng, N, list(rng.integers(1, 200, size=12)) +
                                           [1] * 40))]
     for name, idx in batches:
         w = W.with_idx(base, idx)
@@ -190,12 +191,15 @@ def test_rank128_thousand_adapters_large_shape(P, scale):
     check_counters(rd)
 
 
-def test_unusable_entries_are_counted(P):
+@pytest.mark.parametrize("reps", [1, 3])
+def test_unusable_entries_are_counted(P, reps):
     """A rank above max_rank (or below 0) cannot be applied: those tokens keep
     y_base, the workspace counts them once per call, the rest of the batch is
-    the oracle's, and plora_check_adapters names the first such entry."""
+    the oracle's, and plora_check_adapters names the first such entry.  With
+    the lengths three times over (525 tokens) the apply takes its two-part
+    form, whose expand work groups do the counting."""
     w = W.make_workload("decode", scale="parity", ranks=16, n_adapters=64,
-                        idx=lengths_idx(np.random.default_rng(5), 64, LENGTHS))
+                        idx=lengths_idx(np.random.default_rng(5), 64, LENGTHS * reps))
     bad = int(w.idx[0])
     ranks = w.ranks.copy()
     ranks[bad] = 24                            # above max_rank = 16
