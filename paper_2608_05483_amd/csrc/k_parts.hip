@@ -1,4 +1,8 @@
 // k_parts.hip -- the two parts of plora_apply for batches above 256 tokens, in one launch.
+// a short segment's adapter (a vector-path tile) is read once per call:
+// non-temporal reads; a long segment's is re-read by each of its tiles
+#define PLORA_ADAPTER_POLICY 2
+#define PLORA_MATRIX_POLICY 0
 #include "plora_dev.h"
 
 namespace plora_impl {

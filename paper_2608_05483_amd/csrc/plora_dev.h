@@ -122,20 +122,29 @@ __device__ __forceinline__ Rsrc block_rsrc(const uint16_t* p, int64_t n) {
 }
 
 // Cache policy of adapter reads, set by each kernel's source file before it
-// includes this header.  The exchange-form kernels read every byte of an
+// includes this header: PLORA_ADAPTER_POLICY for the vector paths (tiles of
+// a few tokens), PLORA_MATRIX_POLICY (by default the same) for the matrix
+// and general-rank paths.  The exchange-form kernels read every byte of an
 // adapter's blocks once per call, so they read them non-temporally (2): the
 // caches then keep what is reused, the kernel's code, the token metadata and
-// the exchange words.  The other forms re-read A_i from the caches, once per
-// column slice or once per tile of a long segment, and keep the default (0).
+// the exchange words.  The two-part form reads a short segment's adapter
+// (one vector-path tile) once too, but re-reads a long segment's A_i and
+// B_i once per tile (matrix path), from the caches; the two-launch form
+// keeps the default (0) throughout.
 #ifndef PLORA_ADAPTER_POLICY
 #define PLORA_ADAPTER_POLICY 0
 #endif
+#ifndef PLORA_MATRIX_POLICY
+#define PLORA_MATRIX_POLICY PLORA_ADAPTER_POLICY
+#endif
 constexpr int kAdapterPolicy = PLORA_ADAPTER_POLICY;
+constexpr int kMatrixPolicy = PLORA_MATRIX_POLICY;
 
-// 16 bytes at element e of the block, zero where !ok.
+// 16 bytes at element e of the block, zero where !ok (POL: the cache policy).
+template <int POL = kAdapterPolicy>
 __device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
   const i32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? (int)(e * 2) : kPastEnd, 0,
-                                                          kAdapterPolicy);
+                                                          POL);
   return make_uint4((uint32_t)v.x, (uint32_t)v.y, (uint32_t)v.z, (uint32_t)v.w);
 }
 
@@ -1181,7 +1190,7 @@ __device__ __forceinline__ void shrink_mfma(const ApplyArgs& g, const Tile& t, c
       const bool ok = row < rows && oc * 8 < t.r;
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void*)(asrc + (ok ? row * t.r + oc * 8 : 0)),
-          (__attribute__((address_space(3))) void*)(base + 64 * i * 16), 16, 0, kAdapterPolicy);
+          (__attribute__((address_space(3))) void*)(base + 64 * i * 16), 16, 0, kMatrixPolicy);
     }
 #pragma unroll
     for (int i = 0; i < NXI; ++i) {
@@ -1349,7 +1358,7 @@ __device__ __forceinline__ void expand_load_b(const ApplyArgs& g, const Tile& t,
   for (int j = 0; j < 8; ++j) {
     const int q = (int)threadIdx.x + j * kNT;
     const int c = q / per_row, col = q - c * per_row;
-    pre.breg[j] = bld16(rb, (int64_t)c * g.h_out + j0 + col * 8, q < n16);
+    pre.breg[j] = bld16<kMatrixPolicy>(rb, (int64_t)c * g.h_out + j0 + col * 8, q < n16);
   }
 }
 
@@ -1619,7 +1628,7 @@ __device__ __forceinline__ void shrink_gen(const ApplyArgs& g, const Tile& t, co
 #pragma unroll
     for (int i = 0; i < kGA; ++i) {
       const int q = tid + i * kNT;
-      ar[i] = bld16(ra, (int64_t)w0 * r + q * 8, q < n16);
+      ar[i] = bld16<kMatrixPolicy>(ra, (int64_t)w0 * r + q * 8, q < n16);
     }
 #pragma unroll
     for (int i = 0; i < kGX; ++i) {
