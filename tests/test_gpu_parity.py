@@ -395,6 +395,12 @@ def test_two_part_fallback_meets_the_bars(P):
     yref, yout = oracle_y(w)
     check_y(y, yref, yout, w, strict_l2=True)
     assert (run.apply() == run.expand(run.shrink())).all()
+    # every call, the one that gave up waiting included, leaves the
+    # readiness words (4096 64-bit words after the 336 epochs and the two
+    # counters, 256-byte aligned) at zero
+    off = (336 * 8 + 2 * 8 + 255) // 256 * 256
+    torch.cuda.synchronize()
+    assert int(run.ws.buf[off:off + 4096 * 8].count_nonzero()) == 0
 
 
 def test_two_launches_above_the_readiness_words(P):
@@ -460,12 +466,14 @@ def test_workspace_shared_across_batches_and_stacks(P):
         check_y(bits16(y), yref, yout, ww, strict_l2=True)
 
 
-def test_apply_graph_replay(P):
+@pytest.mark.parametrize("name", ["decode", "ragged"])
+def test_apply_graph_replay(P, name):
     """plora_apply captured in a graph and replayed (the exchange's epochs
-    live on the device, so every replay gets fresh tags), with eager calls
-    between the replays and new x each time; every replay equals the eager
-    call on the same inputs bit for bit."""
-    w = workload("decode", "parity")
+    live on the device, so every replay gets fresh tags; above 256 tokens
+    every call leaves the readiness words at zero), with eager calls between
+    the replays and new x each time; every replay equals the eager call on
+    the same inputs bit for bit."""
+    w = workload(name, "parity")
     run = Run(P, w).segment()
     rng = np.random.default_rng(9)
     xs = [run.x.clone()] + [run.x[torch.from_numpy(rng.permutation(w.T)).cuda()].clone()
