@@ -130,7 +130,7 @@ __device__ __forceinline__ Rsrc block_rsrc(const uint16_t* p, int64_t n) {
 // the exchange words.  The two-part form reads a short segment's adapter
 // (one vector-path tile) once too, but re-reads a long segment's A_i and
 // B_i once per tile (matrix path), from the caches; the two-launch form
-// keeps the default (0) throughout.
+// (shrink and expand launches) keeps the default (0) throughout.
 #ifndef PLORA_ADAPTER_POLICY
 #define PLORA_ADAPTER_POLICY 0
 #endif
@@ -172,12 +172,16 @@ __device__ __forceinline__ uint4 bld16(Rsrc r, int64_t e, bool ok) {
 //   its tile; the slices of a tile are numbered onto one XCD, so the first
 //   read brings A_i into that XCD's L2 and the others hit it.
 //
-//   two launches (batches above kFusedTokens tokens): item (tile, h_in
-//   slice) writes its partial v to the workspace; item (tile, column slice)
-//   sums the tile's KS partials in slice order and expands.  Every byte of
-//   A_i, B_i and x is then read by one work group only, and a rank-64 tile's
+//   two parts (batches above kFusedTokens tokens): item (tile, h_in slice)
+//   writes its partial v to the workspace; item (tile, column slice) sums
+//   the tile's KS partials in slice order and expands.  Every byte of A_i,
+//   B_i and x is then read by one work group only, and a rank-64 tile's
 //   stream of A_i is split over KS items (the one-launch form above measured
-//   79.5 us on the ragged workload of 512 tokens, against 73 for this one).
+//   79.5 us on the ragged workload of 512 tokens, against 73 for this one as
+//   two launches).  The two parts run as one launch (parts_kernel, the
+//   expand items starting on a tile once its partials are stored), or as a
+//   shrink launch and an expand launch for a batch with more tile slots than
+//   the workspace has readiness words.
 //
 // Grids are sized on the host for the most items any tile count up to the
 // capacity can produce; surplus work groups return after one load.
@@ -224,8 +228,8 @@ constexpr int kWGPerCU = 2;          // resident work groups per compute unit
 // masked slot still costs address cycles ahead of the real ones: the
 // one-launch forms (decode-sized slices) request 4 (decode 14.3 us per
 // launch with 16, 13.6 with 8, 13.15 with 4; the large batch 49.7, 50.1,
-// 49.5), the two-launch forms 8 (ragged 62.9 with 16, 62.1 with 8, 62.8 with
-// 4).  A kernel file sets PLORA_PREFETCH_CHUNKS before including this header.
+// 49.5), the two-part forms 8 (ragged 62.9 with 16, 62.1 with 8, 62.8 with
+// 4, as two launches; in one launch 60.5 with 8, 60.9 with 4).  A kernel file sets PLORA_PREFETCH_CHUNKS before including this header.
 #ifndef PLORA_PREFETCH_CHUNKS
 #define PLORA_PREFETCH_CHUNKS 8
 #endif
@@ -309,9 +313,9 @@ struct Tile {
 
 // The slices of one call: n_tiles tiles (as written by plora_segment),
 // rounded up to a multiple of 8, times KS slices of KR rows of h_in (a
-// multiple of 64, the last one shorter) for the shrink launch, or times JS
+// multiple of 64, the last one shorter) for the shrink items, or times JS
 // slices of W y columns (a multiple of 16, the last one shorter) for the
-// expand launch.  KS and JS are the slot count over the rounded tile count,
+// expand items.  KS and JS are the slot count over the rounded tile count,
 // to nearest, within [1, ks_max] and [1, js_max]; so a launch has at most
 // max(4/3 slots, rounded tile count) items and at most ks_max (js_max) times
 // the rounded tile count, whichever is less (the host sizes grids by that).
@@ -416,7 +420,7 @@ __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, in
 // chip; giving each XCD a contiguous range of tiles instead measured 10 us
 // slower on the ragged workload.
 //
-// In the two-launch form, an order that sends a long segment's consecutive
+// In the two-part form, an order that sends a long segment's consecutive
 // tiles (with one slice) to one XCD, so that its slice of A_i is fetched from
 // HBM once and then hit in that XCD's L2, cut the prefill shrink's HBM reads
 // by 30% but not its time, and made the ragged workload 1.5 us slower.
@@ -962,7 +966,7 @@ __device__ __forceinline__ void exchange_item(int b, int S, int& q, int& s) {
 }
 
 // Publish this item's partial v (sm.vs) and replace sm.vs by the sum of all
-// S partials, in slice order (the order plora_shrink and the two-launch form
+// S partials, in slice order (the order plora_shrink and the two-part form
 // sum them in).  Entry o = l r + c of the tile keeps its kMaxSlices words
 // side by side, so one address serves all of them.  A word carrying this
 // call's tag never changes again during the call, so a poll simply reloads
@@ -2141,7 +2145,7 @@ __device__ __forceinline__ float sum_parts(const ApplyArgs& g, const Plan& p, co
   return v;
 }
 
-// The expand launch's v: each entry summed from the partials as sum_parts
+// The expand items' v: each entry summed from the partials as sum_parts
 // sums it (slice order, the same bits), with the loads of kSumBatch entries
 // per thread (every slice of each) issued before any is added, so that a
 // tile costs one memory round trip per batch rather than one per entry
