@@ -104,10 +104,12 @@ typedef enum {
 /* Largest token batch one plora_segment call groups. */
 #define PLORA_MAX_TOKENS 16384
 /* Tokens per work tile: a segment longer than this is split into tiles.
- * Batches of up to 256 tokens are tiled PLORA_SMALL_BATCH_TILE_TOKENS tokens
- * at a time, larger ones PLORA_TILE_TOKENS at a time. */
+ * Batches of up to 64 tokens are tiled PLORA_DECODE_TILE_TOKENS tokens at a
+ * time, batches of 65 to 256 tokens PLORA_SMALL_BATCH_TILE_TOKENS at a time,
+ * larger ones PLORA_TILE_TOKENS at a time. */
 #define PLORA_TILE_TOKENS 32
 #define PLORA_SMALL_BATCH_TILE_TOKENS 2
+#define PLORA_DECODE_TILE_TOKENS 1
 /* Most projections one plora_apply_multi call serves. */
 #define PLORA_MAX_PROJECTIONS 8
 /* Entries of plora_segments.meta. */

@@ -22,7 +22,8 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   const uint64_t ep = xload(g.xep + u);
-  if (g.T <= 64) {
+  static_assert(kDecodeTokens == 64, "wave_segment ranks one wavefront's tokens");
+  if (g.T <= kDecodeTokens) {
     if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
   } else {
     block_segment(g, idx, u, so, blockIdx.x == 0, lt);

@@ -38,14 +38,24 @@ constexpr int kTT = PLORA_TILE_TOKENS;   // most tokens per tile
 static_assert((kTT & (kTT - 1)) == 0, "tile positions are taken modulo kTT with a mask");
 constexpr int kFusedTokens = 256;    // largest batch plora_apply runs as one launch
 // Tokens per tile by batch size.  Batches of up to kFusedTokens tokens (the
-// one-launch forms: decode) are cut into tiles of kSmallTile tokens, which the
+// one-launch forms) are cut into tiles of kSmallTile tokens, which the
 // vector path takes at every rank: with tiles of up to kTT tokens, a hot
 // adapter's tile of 3 to 14 tokens took the matrix path and finished about
 // 3 us after the single-token tiles, setting the launch's length.  A hot
 // adapter then has several tiles that read its blocks at the same time (the
-// repeats are cache hits).  Larger batches keep tiles of kTT tokens.
+// repeats are cache hits).  Batches of up to kDecodeTokens tokens (decode)
+// take single-token tiles: every item then has the same chain of loads, and
+// the decode workload's launch went from 13.07 to 12.15 us; at 256 tokens
+// (rank 64, two slices per tile, each item reading half of A_i) the repeats
+// cost more than they save (49.4 -> 52.4 us), so larger one-launch batches
+// keep tiles of two.  Batches above kFusedTokens take tiles of kTT tokens.
 constexpr int kSmallTile = PLORA_SMALL_BATCH_TILE_TOKENS;
-__host__ __device__ constexpr int tile_tokens(int T) { return T <= kFusedTokens ? kSmallTile : kTT; }
+constexpr int kDecodeTile = PLORA_DECODE_TILE_TOKENS;
+constexpr int kDecodeTokens = 64;
+static_assert(kDecodeTile <= kSmallTile, "the exchange regions hold kSmallTile tokens");
+__host__ __device__ constexpr int tile_tokens(int T) {
+  return T <= kDecodeTokens ? kDecodeTile : T <= kFusedTokens ? kSmallTile : kTT;
+}
 constexpr int kSegThreads = 1024;
 constexpr int kSegWaves = kSegThreads / 64;
 // Groups of 64 words per wave in the radix passes: each wave owns a chunk of
@@ -1990,7 +2000,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const int sstart = vp ? 63 - __clzll(smask & upto) : 0;
   const uint64_t later = smask & ~upto;
   const int send = later ? __ffsll((long long)later) - 1 : n_valid;   // segment end
-  const bool tflag = vp && ((lane - sstart) % kSmallTile) == 0;
+  const bool tflag = vp && ((lane - sstart) % kDecodeTile) == 0;
   const uint64_t tmask = __ballot(tflag);
   const int tu = __popcll(tmask & below);                 // tile starting here
   const int n_tiles = min(__popcll(tmask), so.tile_cap);
@@ -2003,7 +2013,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
     for (int q = n_seg + lane; q <= so.cap; q += 64) so.seg_ptr[q] = n_valid;
     for (int q = n_seg + lane; q < so.cap; q += 64) so.seg_id[q] = -1;
     if (tflag && tu < so.tile_cap)
-      so.tiles[tu] = make_int4(kp, lane, min(kSmallTile, send - lane), cur);
+      so.tiles[tu] = make_int4(kp, lane, min(kDecodeTile, send - lane), cur);
     for (int q = n_tiles + lane; q < so.tile_cap; q += 64) so.tiles[q] = make_int4(-1, 0, 0, -1);
     if (lane < 8)
       so.meta[lane] = lane == 0 ? n_seg : lane == 1 ? n_valid : lane == 2 ? n_none
@@ -2015,7 +2025,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const int p0 = mine ? __ffsll((long long)mine) - 1 : 0;
   const uint64_t after0 = smask & (p0 == 63 ? 0 : ~((uint64_t(2) << p0) - 1));
   const int end0 = after0 ? __ffsll((long long)after0) - 1 : n_valid;
-  const int L = mine ? min(kSmallTile, end0 - p0) : 0;
+  const int L = mine ? min(kDecodeTile, end0 - p0) : 0;
   lt.rank_of[lane] = m_r;
   lt.scale_of[lane] = m_s;
   lt.ao_of[lane] = m_ao;

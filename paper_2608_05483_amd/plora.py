@@ -25,10 +25,13 @@ PLORA_MAX_RANK = 128
 PLORA_MAX_TOKENS = 16384
 PLORA_TILE_TOKENS = 32
 PLORA_SMALL_BATCH_TILE_TOKENS = 2
+PLORA_DECODE_TILE_TOKENS = 1
 
 
 def tile_tokens(T: int) -> int:
     """Tokens per tile of a batch of T tokens (include/plora.h)."""
+    if T <= 64:
+        return PLORA_DECODE_TILE_TOKENS
     return PLORA_SMALL_BATCH_TILE_TOKENS if T <= 256 else PLORA_TILE_TOKENS
 PLORA_META_WORDS = 8
 PLORA_MAX_PROJECTIONS = 8

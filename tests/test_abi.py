@@ -47,10 +47,14 @@ def test_tile_capacity():
     assert P.plora_tile_capacity(0, 10) == 0
     assert P.plora_tile_capacity(64, 1000) == 64
     assert P.plora_tile_capacity(8192, 32) == 32 + 8192 // 32
-    assert P.plora_tile_capacity(5, 1) == 3            # tiles of 2 tokens up to 256
+    assert P.plora_tile_capacity(5, 1) == 5            # tiles of 1 token up to 64
+    assert P.plora_tile_capacity(64, 1) == 64
+    assert P.plora_tile_capacity(65, 1) == 1 + 65 // 2  # tiles of 2 tokens up to 256
+    assert P.plora_tile_capacity(256, 1) == 1 + 128
     assert P.plora_tile_capacity(300, 1) == 1 + 300 // 32
+    assert [P.tile_tokens(T) for T in (1, 64, 65, 256, 257)] == [1, 1, 2, 2, 32]
     # the bound holds for the worst batch: every segment of length Kk+1
-    for T, N in [(100, 3), (256, 7), (1000, 7), (16384, 1000)]:
+    for T, N in [(40, 3), (100, 3), (256, 7), (1000, 7), (16384, 1000)]:
         cap = min(T, N)
         K = P.tile_tokens(T)
         assert P.plora_tile_capacity(T, N) >= min(T, cap + T // K)

@@ -235,9 +235,9 @@ def test_overlong_one_launch_tile_is_skipped_and_counted(P):
     y_ref = run.apply()
     tiles = run.segs.tiles.view(-1, 4).cpu().numpy().copy()
     n = int(run.segs.meta[4].item())
-    tl = P.PLORA_SMALL_BATCH_TILE_TOKENS
+    tl = P.tile_tokens(w.T)
     assert n == 40 // tl and (tiles[:n, 2] == tl).all()
-    L = 2 * tl + 1                                  # longer than any one-launch tile
+    L = 2 * P.PLORA_SMALL_BATCH_TILE_TOKENS + 1     # longer than any one-launch tile
     keep = tiles[:n][tiles[:n, 1] >= L + 1]         # the tiles after positions 0..L
     new = [(7, 0, L, 0), (7, L, 1, 0)] + [tuple(t) for t in keep]
     tiles[:] = (-1, 0, 0, -1)
