@@ -21,12 +21,13 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
   __shared__ LocalTile lt;
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
-  const uint64_t ep = xload(g.xep + u);
+  uint64_t ep = 0;
   static_assert(kDecodeTokens == 64, "wave_segment ranks one wavefront's tokens");
   if (g.T <= kDecodeTokens) {
-    if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt);
+    // (only thread 0 keeps the epoch, in the item's stash)
+    if (threadIdx.x < 64) wave_segment(g, idx, u, so, blockIdx.x == 0, lt, ep);
   } else {
-    block_segment(g, idx, u, so, blockIdx.x == 0, lt);
+    block_segment(g, idx, u, so, blockIdx.x == 0, lt, ep);
   }
   lds_sync();
   apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {

@@ -1943,6 +1943,20 @@ struct LocalTile {
   int64_t ao_of[kSegApplyMax], bo_of[kSegApplyMax];
 };
 
+// The tile slot's exchange epoch, requested right after the ids and before
+// they are waited for: the vector-memory counter retires in order, so an
+// epoch requested first (an agent-scope load, which goes to memory) held up
+// the ids' wait behind it, and one requested after that wait added its trip
+// to the metadata's.  The empty asm statements keep the epoch's request
+// between the id's request and its first use (the second one takes the id
+// as an operand, so nothing that uses it can move above the request).
+__device__ __forceinline__ uint64_t epoch_after_ids(const ApplyArgs& g, int u, int& id) {
+  __asm__ volatile("" ::: "memory");
+  const uint64_t ep = xload(g.xep + u);
+  __asm__ volatile("" : "+v"(id) : : "memory");
+  return ep;
+}
+
 // The segmentation of a batch of T <= 64 tokens by one wavefront, the same
 // function plora_segment computes: tokens ordered by (adapter id, token
 // index), ids outside [0, N) after every valid one.  Each lane holds the
@@ -1956,11 +1970,14 @@ struct LocalTile {
 // (A bitonic sort over lane shuffles measured about 1 us: 21 dependent
 // cross-lane permutes.)
 __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* idx, int u,
-                                             const SegOut& so, bool write, LocalTile& lt) {
+                                             const SegOut& so, bool write, LocalTile& lt,
+                                             uint64_t& ep) {
   const int T = g.T, N = g.N;
   const int lane = threadIdx.x & 63;
   const bool in = lane < T;
-  const int id = in ? idx[lane] : 0;
+  int id_in = idx[in ? lane : 0];           // (T >= 1: no branch, so no wait here)
+  ep = epoch_after_ids(g, u, id_in);
+  const int id = in ? id_in : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
   const bool invalid = in && !valid && !none;
@@ -2047,12 +2064,15 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
 // (counts for the indices, the last and first start for the segment that
 // spans a wavefront boundary).  Every thread of the work group calls it.
 __device__ __forceinline__ void block_segment(const ApplyArgs& g, const int32_t* idx, int u,
-                                              const SegOut& so, bool write, LocalTile& lt) {
+                                              const SegOut& so, bool write, LocalTile& lt,
+                                              uint64_t& ep) {
   constexpr int NW = kNT / 64;
   const int T = g.T, N = g.N;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const bool in = tid < T;
-  const int id = in ? idx[tid] : 0;
+  int id_in = idx[in ? tid : 0];            // (T >= 1: no branch, so no wait here)
+  ep = epoch_after_ids(g, u, id_in);
+  const int id = in ? id_in : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
   const bool invalid = in && !valid && !none;
