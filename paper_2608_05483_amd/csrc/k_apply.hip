@@ -15,13 +15,23 @@ namespace plora_impl {
 __global__ __launch_bounds__(kNT, kWGPerCU) void apply_kernel(ApplyArgs g) {
   extern __shared__ __align__(16) unsigned char apply_lds[];
   __shared__ ItemStash stash;
+  request_adapter_args(g);
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   // the slot's epoch is requested together with the tile record (the host
-  // made sure the slot count is at most kXSlots)
-  const uint64_t ep = xload(g.xep + u);
-  apply_item(g, s, u, ep, stash, apply_lds,
-             [&](Tile& t, int& my_tok) { return load_tile(g, u, t, my_tok); });
+  // made sure the slot count is at most kXSlots); apply_item reads it once
+  // the tile is loaded
+  uint64_t ep = 0;
+  apply_item(g, s, u, ep, stash, apply_lds, [&](Tile& t, int& my_tok) {
+    // load_tile, with the epoch requested right after the tile record
+    t.bad = false;
+    if (u >= g.tile_cap) return false;
+    int4 ti = g.tiles[u];
+    ep = epoch_after(g, u, ti.x);
+    if (!tile_from_record(g, ti, t)) return false;
+    my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
+    return tile_adapter(g, t, my_tok);
+  });
 }
 
 void launch_apply(const ApplyArgs& g, unsigned grid, size_t lds, hipStream_t stream) {

@@ -19,6 +19,7 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void segment_apply_kernel(ApplyArgs 
   extern __shared__ __align__(16) unsigned char apply_lds[];
   __shared__ ItemStash stash;
   __shared__ LocalTile lt;
+  request_adapter_args(g);
   int u, s;
   exchange_item((int)blockIdx.x, g.fixed_slices, u, s);
   uint64_t ep = 0;

@@ -406,6 +406,13 @@ __device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& m
   return tile_blocks(g, t, my_tok, ao, bo);
 }
 
+// The adapter, first position and length of a tile from its record; false
+// for padding entries and records out of range.
+__device__ __forceinline__ bool tile_from_record(const ApplyArgs& g, const int4& ti, Tile& t) {
+  t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
+  return t.a >= 0 && t.a < g.N && t.L > 0 && t.L <= kTT && t.p0 >= 0 && t.p0 + t.L <= g.T;
+}
+
 // Read and validate tile u.  Returns false (for the whole work group) for
 // padding entries and for adapters the kernels must skip.  Threads below L
 // also fetch their tile row's token index (-1 if unusable); it is issued
@@ -413,10 +420,7 @@ __device__ __forceinline__ bool tile_adapter(const ApplyArgs& g, Tile& t, int& m
 __device__ __forceinline__ bool load_tile(const ApplyArgs& g, int u, Tile& t, int& my_tok) {
   t.bad = false;
   if (u < 0 || u >= g.tile_cap) return false;
-  const int4 ti = g.tiles[u];
-  t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
-  if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T)
-    return false;
+  if (!tile_from_record(g, g.tiles[u], t)) return false;
   my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
   return tile_adapter(g, t, my_tok);
 }
@@ -1845,7 +1849,7 @@ __device__ __forceinline__ void plain_v(const ApplyArgs& g, const Tile& t, const
 // (adapter, first position, length) and this thread's token, false for a
 // slot without a usable tile.
 template <class Src>
-__device__ __forceinline__ void apply_item(const ApplyArgs& g, int s, int slot, uint64_t ep,
+__device__ __forceinline__ void apply_item(const ApplyArgs& g, int s, int slot, const uint64_t& ep,
                                            ItemStash& stash, unsigned char* lds, Src&& src) {
   {
     Tile t;
@@ -1947,18 +1951,27 @@ struct LocalTile {
   int64_t ao_of[kSegApplyMax], bo_of[kSegApplyMax];
 };
 
-// The tile slot's exchange epoch, requested right after the ids and before
-// they are waited for: the vector-memory counter retires in order, so an
-// epoch requested first (an agent-scope load, which goes to memory) held up
-// the ids' wait behind it, and one requested after that wait added its trip
-// to the metadata's.  The empty asm statements keep the epoch's request
-// between the id's request and its first use (the second one takes the id
-// as an operand, so nothing that uses it can move above the request).
-__device__ __forceinline__ uint64_t epoch_after_ids(const ApplyArgs& g, int u, int& id) {
+// The tile slot's exchange epoch, requested right after the item's first
+// load (the ids, or the tile record) and before that load is waited for:
+// the vector-memory counter retires in order, so an epoch requested first
+// (an agent-scope load, which goes to memory) held up the first load's wait
+// behind it, and one requested after that wait added its trip to the next
+// load's.  The empty asm statements keep the epoch's request between the
+// first load's request and its first use (the second one takes the loaded
+// value as an operand, so nothing that uses it can move above the request).
+__device__ __forceinline__ uint64_t epoch_after(const ApplyArgs& g, int u, int& first) {
   __asm__ volatile("" ::: "memory");
   const uint64_t ep = xload(g.xep + u);
-  __asm__ volatile("" : "+v"(id) : : "memory");
+  __asm__ volatile("" : "+v"(first) : : "memory");
   return ep;
+}
+
+// The adapter-stack arguments that an item's first steps read (tile_blocks),
+// requested at the kernel's entry with the others: requested at their first
+// use, their scalar-cache miss held up that step (decode 12.01 -> 11.85 us).
+__device__ __forceinline__ void request_adapter_args(const ApplyArgs& g) {
+  __asm__ volatile("" ::"s"(g.A), "s"(g.B), "s"(g.a_len), "s"(g.b_len), "s"(g.A_pool),
+                   "s"(g.B_pool));
 }
 
 // The segmentation of a batch of T <= 64 tokens by one wavefront, the same
@@ -1980,7 +1993,7 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const int lane = threadIdx.x & 63;
   const bool in = lane < T;
   int id_in = idx[in ? lane : 0];           // (T >= 1: no branch, so no wait here)
-  ep = epoch_after_ids(g, u, id_in);
+  ep = epoch_after(g, u, id_in);
   const int id = in ? id_in : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
@@ -2075,7 +2088,7 @@ __device__ __forceinline__ void block_segment(const ApplyArgs& g, const int32_t*
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const bool in = tid < T;
   int id_in = idx[in ? tid : 0];            // (T >= 1: no branch, so no wait here)
-  ep = epoch_after_ids(g, u, id_in);
+  ep = epoch_after(g, u, id_in);
   const int id = in ? id_in : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
@@ -2248,9 +2261,7 @@ __global__ __launch_bounds__(kNT, kWGPerCU) void expand_kernel(ApplyArgs g) {
     const int u = item_slot(p, kColSlices, blockIdx.x, js);
     t.bad = false;
     if (u >= p.n_tiles || u >= g.tile_cap) return;
-    const int4 ti = g.tiles[u];
-    t.a = ti.x; t.p0 = ti.y; t.L = ti.z;
-    if (t.a < 0 || t.a >= g.N || t.L <= 0 || t.L > kTT || t.p0 < 0 || t.p0 + t.L > g.T) return;
+    if (!tile_from_record(g, g.tiles[u], t)) return;
     PartBatch pb;
     parts_issue(g, p.KS, t.p0, t.L, 0, pb);
     my_tok = (int)threadIdx.x < t.L ? g.perm[t.p0 + threadIdx.x] : -1;
