@@ -441,6 +441,34 @@ def test_workspace_across_large_batches(P):
         check_y(bits16(y), yref, yout, ww, strict_l2=True)
 
 
+def test_two_part_repeated_calls_bitwise(P):
+    """Sixteen two-part calls in a row on one workspace, each with a new draw
+    of ids and activations: every one gives the split calls' bits (a stale
+    partial read through the readiness words would not), and no expand
+    item gives up waiting."""
+    w = workload("ragged", "paper")
+    ad = P.Adapters.from_workload(w)
+    ws = P.Workspace(1024, ad)
+    seed = 1000 + W.CONFIG_NAMES.index("ragged")
+    for k in range(16):
+        idx = W.draw_idx("ragged", seed, k)
+        ww = W.with_idx(w, idx)
+        say(f"two-part repeated call {k}: T={idx.size}")
+        segs = P.Segments(idx.size, w.n_adapters)
+        P.segment(dev(idx), segs)
+        x = dev(np.ascontiguousarray(ww.x).view(np.int16))
+        y0 = dev(np.ascontiguousarray(ww.y_base).view(np.int16))
+        y = y0.clone()
+        P.apply(x, ad, segs, y, ws)
+        v = torch.empty((idx.size, ad.max_rank), dtype=torch.float32, device="cuda")
+        P.shrink(x, ad, segs, v, ws)
+        y2 = y0.clone()
+        P.expand(v, ad, segs, y2)
+        torch.cuda.synchronize()
+        assert torch.equal(y, y2), k
+    assert ws.counters() == (0, 0)
+
+
 def test_workspace_shared_across_batches_and_stacks(P):
     """One workspace serving one-launch calls of varying batch size and of two
     adapter stacks (ranks 16 and 64) in turn: its exchange regions and epochs
