@@ -1991,35 +1991,25 @@ __device__ __forceinline__ void request_adapter_args(const ApplyArgs& g) {
 }
 
 // The segmentation of a batch of T <= 64 tokens by one wavefront, the same
-// function plora_segment computes: tokens ordered by (adapter id, token
-// index), ids outside [0, N) after every valid one.  Each lane holds the
-// word (key << 6) | t of one token (key = id, N for a skipped token, N + 1
-// past T).  The words are distinct, so each one's rank (how many words are
-// smaller, counted against all 64 read back from LDS) is its sorted
-// position, and there is exactly one order.  Segments start where the key
-// changes, tiles every kTT positions into a segment.  With `write`, the
+// function plora_segment computes, written to so: tokens ordered by
+// (adapter id, token index), ids outside [0, N) after every valid one.  Each
+// lane holds the word (key << 6) | t of one token (key = id, N for a skipped
+// token, N + 1 past T).  The words are distinct, so each one's rank (how many
+// words are smaller, counted against all 64 read back from LDS) is its
+// sorted position, and there is exactly one order.  Segments start where the
+// key changes, tiles every kDecodeTile positions into a segment.  The
 // wavefront stores every output of plora_segment (perm, seg_ptr, seg_id,
-// tiles and meta, unused tails included); every caller gets tile u in lt.
-// (A bitonic sort over lane shuffles measured about 1 us: 21 dependent
-// cross-lane permutes.)
-__device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* idx, int u,
-                                             const SegOut& so, bool write, LocalTile& lt,
-                                             uint64_t& ep) {
+// tiles and meta, unused tails included).  (A bitonic sort over lane
+// shuffles measured about 1 us: 21 dependent cross-lane permutes.)
+__device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* idx,
+                                             const SegOut& so, LocalTile& lt) {
   const int T = g.T, N = g.N;
   const int lane = threadIdx.x & 63;
   const bool in = lane < T;
-  int id_in = idx[in ? lane : 0];           // (T >= 1: no branch, so no wait here)
-  ep = epoch_after(g, u, id_in);
-  const int id = in ? id_in : 0;
+  const int id = in ? idx[lane] : 0;
   const bool valid = in && id >= 0 && id < N;
   const bool none = in && id == -1;
   const bool invalid = in && !valid && !none;
-  // the metadata of this token's adapter, requested now so that its trip
-  // overlaps the ranking (lanes without an adapter read adapter 0's, unused)
-  const int ida = valid ? id : 0;
-  const int m_r = g.ranks[ida];
-  const float m_s = g.scales[ida];
-  const int64_t m_ao = g.a_off[ida], m_bo = g.b_off[ida];
   const uint32_t key = valid ? (uint32_t)id : (uint32_t)N + (in ? 0u : 1u);
   const uint32_t w = (key << 6) | (uint32_t)lane;
   // LDS traffic of one wavefront is processed in order, so each read below
@@ -2054,40 +2044,19 @@ __device__ __forceinline__ void wave_segment(const ApplyArgs& g, const int32_t* 
   const uint64_t tmask = __ballot(tflag);
   const int tu = __popcll(tmask & below);                 // tile starting here
   const int n_tiles = min(__popcll(tmask), so.tile_cap);
-  if (write) {
-    if (in) so.perm[lane] = vp ? tp : -1;
-    if (sflag) {
-      so.seg_ptr[cur] = lane;
-      so.seg_id[cur] = kp;
-    }
-    for (int q = n_seg + lane; q <= so.cap; q += 64) so.seg_ptr[q] = n_valid;
-    for (int q = n_seg + lane; q < so.cap; q += 64) so.seg_id[q] = -1;
-    if (tflag && tu < so.tile_cap)
-      so.tiles[tu] = make_int4(kp, lane, min(kDecodeTile, send - lane), cur);
-    for (int q = n_tiles + lane; q < so.tile_cap; q += 64) so.tiles[q] = make_int4(-1, 0, 0, -1);
-    if (lane < 8)
-      so.meta[lane] = lane == 0 ? n_seg : lane == 1 ? n_valid : lane == 2 ? n_none
-                    : lane == 3 ? n_invalid : lane == 4 ? n_tiles : 0;
+  if (in) so.perm[lane] = vp ? tp : -1;
+  if (sflag) {
+    so.seg_ptr[cur] = lane;
+    so.seg_id[cur] = kp;
   }
-  // tile u starts at the u-th tile start p0 and ends at kTT positions or at
-  // the end of its segment
-  const uint64_t mine = __ballot(tflag && tu == u && u < n_tiles);
-  const int p0 = mine ? __ffsll((long long)mine) - 1 : 0;
-  const uint64_t after0 = smask & (p0 == 63 ? 0 : ~((uint64_t(2) << p0) - 1));
-  const int end0 = after0 ? __ffsll((long long)after0) - 1 : n_valid;
-  const int L = mine ? min(kDecodeTile, end0 - p0) : 0;
-  lt.rank_of[lane] = m_r;
-  lt.scale_of[lane] = m_s;
-  lt.ao_of[lane] = m_ao;
-  lt.bo_of[lane] = m_bo;
-  if (lane == 0) {
-    const uint32_t s0 = lt.sorted[p0];
-    lt.a = (int)(s0 >> 6);
-    lt.p0 = p0;
-    lt.L = L;
-    lt.t0 = (int)(s0 & 63);        // the tile's first token: its adapter's metadata
-    lt.tmask = 63u;
-  }
+  for (int q = n_seg + lane; q <= so.cap; q += 64) so.seg_ptr[q] = n_valid;
+  for (int q = n_seg + lane; q < so.cap; q += 64) so.seg_id[q] = -1;
+  if (tflag && tu < so.tile_cap)
+    so.tiles[tu] = make_int4(kp, lane, min(kDecodeTile, send - lane), cur);
+  for (int q = n_tiles + lane; q < so.tile_cap; q += 64) so.tiles[q] = make_int4(-1, 0, 0, -1);
+  if (lane < 8)
+    so.meta[lane] = lane == 0 ? n_seg : lane == 1 ? n_valid : lane == 2 ? n_none
+                  : lane == 3 ? n_invalid : lane == 4 ? n_tiles : 0;
 }
 
 // The same function for 64 < T <= kSegApplyMax tokens by the whole work
