@@ -302,9 +302,10 @@ plora_status plora_apply(const uint16_t* x, int64_t ldx,
  * layers can call plora_apply with it).  Arguments as for the two calls;
  * idx is int32 [T] device memory.  For T <= 256 in plora_apply's split
  * exchange form (and 1 <= N < 2^26 - 1 up to 64 tokens, N < 2^24 - 1 above)
- * this is one launch: every work group segments the batch itself (the
- * grouping of section VI-B; one wavefront up to 64 tokens, the whole work
- * group above) and applies its own tile, and one of them also writes seg.
+ * this is one launch: above 64 tokens every work group segments the batch
+ * itself (the grouping of section VI-B) and applies its own tile; up to 64
+ * tokens (single-token tiles) every work group applies its own token
+ * directly; one work group also writes seg.
  * Otherwise it makes the two calls.  y gets the bits plora_apply would give
  * after plora_segment (with the same exception for a partner that never
  * publishes).  Errors as for the two calls.
